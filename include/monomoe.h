@@ -1,0 +1,157 @@
+/*
+ * monomoe.h -- C ABI of the MI355X (gfx950) fused routed-MoE decode operator.
+ *
+ * The operator is the complete routed Mixture-of-Experts layer of MonoMoE
+ * (arXiv 2609.04244) for block-wise FP8 experts, at decode token counts:
+ *   router logits -> softmax + top-k -> per-token, per-128-group dynamic E4M3
+ *   quantisation of the input -> block-FP8 gate/up projection -> SiLU(gate)*up ->
+ *   requantisation -> block-FP8 down projection -> top-k weighted reduction,
+ * all inside ONE persistent kernel launch (paper Sec. 3, "MonoMoE Design": a single
+ * kernel with four logical stages linked by readiness flags).
+ *
+ * The operator interface follows the paper's generic form (Sec. 3.4): the model shape
+ * is fixed per plan, the token count is part of the plan's shape, top-k and the
+ * routing policy (softmax, with or without renormalisation, optional per-expert logit
+ * bias) are plan parameters; X is the input tile, R the routing inputs (router weight
+ * and optional bias), W_gu/W_down the expert weights and S their block scales.
+ *
+ * Conventions for every entry point:
+ *  - All tensor pointers are DEVICE pointers owned by the caller.  The library never
+ *    frees them and never keeps them beyond the work it enqueues.
+ *  - Tensor pointers must be 16-byte aligned and tensors densely packed, row-major.
+ *  - Entry points return MONOMOE_OK (0) or a negative monomoe_status_t.  An argument
+ *    error enqueues nothing.
+ *  - monomoe_forward() and monomoe_forward_debug() never synchronise, never allocate,
+ *    and enqueue exactly one kernel on the given stream, so they can be captured into a
+ *    HIP graph.  A plan owns device workspace: one plan must not be used by two launches
+ *    that can overlap (use one plan per stream).
+ *  - The kernel reports failures it detects on the device (a bounded wait that expired)
+ *    through a status word read with monomoe_plan_status().
+ */
+#ifndef MONOMOE_H
+#define MONOMOE_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* T: tokens per decode step (0..16; T == 0 makes forward a no-op).
+ * H: hidden size, I: expert intermediate size, both multiples of 128 from the set of
+ * compiled shapes (monomoe_supported_shape()).  E: routed experts (1..512). */
+typedef struct {
+    int32_t T, H, E, I;
+} monomoe_shape_t;
+
+typedef struct monomoe_plan_s* monomoe_plan_t;
+
+typedef enum {
+    MONOMOE_OK = 0,
+    MONOMOE_ERR_INVALID = -1,      /* bad argument: null/misaligned pointer, bad shape, bad topk */
+    MONOMOE_ERR_UNSUPPORTED = -2,  /* valid but not compiled: (H,I) pair, T > 16, E > 512     */
+    MONOMOE_ERR_OCCUPANCY = -3,    /* the persistent grid cannot be fully resident             */
+    MONOMOE_ERR_HIP = -4,          /* a HIP runtime call failed                                */
+    MONOMOE_ERR_TIMEOUT = -5       /* device: a bounded readiness wait expired                 */
+} monomoe_status_t;
+
+/* Create a plan for one shape.  topk in [1, E] and topk <= 16; renorm != 0 renormalises
+ * the selected softmax probabilities to sum to 1.  Allocates and zeroes the plan's device
+ * workspace on the current device (synchronously) and picks the persistent grid:
+ * one workgroup per compute unit, after checking that the occupancy calculator allows
+ * at least one per CU for the plan's LDS footprint (readiness waits need every
+ * workgroup resident; paper Sec. 3.2 "Persistent residency").  *plan_out is set only
+ * on success. */
+int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_plan_t* plan_out);
+
+/* Release a plan and its workspace.  The caller makes sure no enqueued launch that uses
+ * the plan is still pending.  NULL is ignored. */
+void monomoe_plan_destroy(monomoe_plan_t plan);
+
+/* Optional routing input: a per-expert fp32 bias [E] (device pointer, or NULL to remove)
+ * added to the router logits before softmax and selection, so it changes both the
+ * selected experts and their weights.  The pointer is read by every later forward. */
+int monomoe_plan_set_router_bias(monomoe_plan_t plan, const float* bias);
+
+/* The operator (paper Sec. 3.4 interface, Eq. 9 weight-major projections):
+ *   x         bf16  [T,H]                 input token tile
+ *   router_w  bf16  [E,H]                 logits = x . router_w^T (+ bias)
+ *   w13       e4m3fn bytes [E,2I,H]       rows [0,I) gate, rows [I,2I) up, K (=H) contiguous
+ *   w13_scale fp32  [E,2I/128,H/128]      dequantised weight = decode(byte) * block scale
+ *   w2        e4m3fn bytes [E,H,I]        K (=I) contiguous
+ *   w2_scale  fp32  [E,H/128,I/128]
+ *   out       bf16  [T,H]                 fully overwritten (round-to-nearest-even)
+ * Enqueues one kernel on `stream`. */
+int monomoe_forward(monomoe_plan_t plan, const void* x, const void* router_w,
+                    const void* w13, const float* w13_scale,
+                    const void* w2, const float* w2_scale,
+                    void* out, hipStream_t stream);
+
+/* Test hooks.  Every pointer may be NULL.  Pair index p = t*topk + j.
+ *   topk_ids  int32 [T,topk]      selected experts, in selection order (written)
+ *   topk_w    fp32  [T,topk]      their routing weights (written)
+ *   xq        u8    [T,H]         E4M3 codes of the quantised input (written)
+ *   xs        fp32  [T,H/128]     input group scales (written)
+ *   act       fp32  [T*topk,I]    SiLU(gate)*up before requantisation (written)
+ *   aq        u8    [T*topk,I]    requantised activation codes (written)
+ *   as        fp32  [T*topk,I/128] requantisation scales (written)
+ *   out_f32   fp32  [T,H]         the weighted sum before rounding to bf16 (written)
+ *   topk_ids_in / topk_w_in       [T,topk] replace the kernel's own selection (read);
+ *                                 both or neither; ids distinct per token, in [0,E)
+ *   spin_limit_ticks              bound of every readiness wait in 100 MHz ticks
+ *                                 (0 = the default of 2 s)
+ *   fail_flag                     nonzero makes the routing wait target unreachable, so
+ *                                 the kernel takes its timeout path and reports
+ *                                 MONOMOE_ERR_TIMEOUT through monomoe_plan_status(). */
+typedef struct {
+    int32_t* topk_ids;
+    float* topk_w;
+    uint8_t* xq;
+    float* xs;
+    float* act;
+    uint8_t* aq;
+    float* as;
+    float* out_f32;
+    const int32_t* topk_ids_in;
+    const float* topk_w_in;
+    uint64_t spin_limit_ticks;
+    int32_t fail_flag;
+} monomoe_debug_t;
+
+int monomoe_forward_debug(monomoe_plan_t plan, const void* x, const void* router_w,
+                          const void* w13, const float* w13_scale,
+                          const void* w2, const float* w2_scale,
+                          void* out, const monomoe_debug_t* dbg, hipStream_t stream);
+
+/* Device-side status of the plan's last launches: MONOMOE_OK or MONOMOE_ERR_TIMEOUT.
+ * Blocking: copies the status word to the host after a device synchronisation.  The
+ * status is sticky until monomoe_plan_reset(). */
+int monomoe_plan_status(monomoe_plan_t plan);
+
+/* Clear the status word and every readiness counter and accumulator of the plan's
+ * workspace (needed only after a device-side error).  Blocking. */
+int monomoe_plan_reset(monomoe_plan_t plan);
+
+/* Launch geometry and footprint of a plan, for tests and benchmarks. */
+typedef struct {
+    int32_t grid;            /* persistent workgroups                       */
+    int32_t block;           /* threads per workgroup                       */
+    int32_t lds_bytes;       /* dynamic + static LDS per workgroup          */
+    int32_t occupancy;       /* workgroups per CU the occupancy API allows  */
+    int32_t num_cus;
+    int64_t workspace_bytes;
+} monomoe_plan_info_t;
+
+int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info);
+
+/* 1 if (H, I) is one of the compiled shapes, else 0. */
+int monomoe_supported_shape(int32_t H, int32_t I);
+
+/* Static string for a status code. */
+const char* monomoe_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

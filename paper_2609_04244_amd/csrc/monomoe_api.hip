@@ -1,0 +1,260 @@
+// Host runtime behind include/monomoe.h: plan validation, persistent-grid sizing with an
+// occupancy check, workspace ownership and the single-launch forward.
+#include "../../include/monomoe.h"
+#include "monomoe_internal.h"
+
+#include <new>
+#include <string.h>
+
+using namespace monomoe;
+
+struct monomoe_plan_s {
+    monomoe_shape_t shape;
+    int topk;
+    int renorm;
+    const KernelEntry* kern;
+    int device;
+    int num_cus;
+    int occupancy;
+    int grid;
+    int lds_dyn;
+    int lds_static;
+    const float* bias;
+    // workspace (one allocation)
+    void* ws;
+    size_t ws_bytes;
+    uint32_t* ctl;
+    float* logits;
+    uint8_t* xq;
+    float* xs;
+    float* act;
+    float* out_acc;
+};
+
+namespace {
+
+constexpr uint64_t kDefaultSpinTicks = 200000000ull;   // 2 s of the 100 MHz realtime clock
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int zero_workspace(monomoe_plan_s* pl) {
+    if (hipMemset(pl->ws, 0, pl->ws_bytes) != hipSuccess) return MONOMOE_ERR_HIP;
+    if (hipDeviceSynchronize() != hipSuccess) return MONOMOE_ERR_HIP;
+    return MONOMOE_OK;
+}
+
+int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void* w13, const float* w13_scale,
+           const void* w2, const float* w2_scale, void* out, const monomoe_debug_t* dbg, hipStream_t stream) {
+    if (!plan) return MONOMOE_ERR_INVALID;
+    const monomoe_shape_t& s = plan->shape;
+    if (s.T == 0) return MONOMOE_OK;
+    if (!x || !router_w || !w13 || !w13_scale || !w2 || !w2_scale || !out) return MONOMOE_ERR_INVALID;
+    if (!aligned16(x) || !aligned16(router_w) || !aligned16(w13) || !aligned16(w2) || !aligned16(out) ||
+        !aligned16(w13_scale) || !aligned16(w2_scale))
+        return MONOMOE_ERR_INVALID;
+
+    KParams p;
+    memset(&p, 0, sizeof p);
+    p.x = static_cast<const uint16_t*>(x);
+    p.rw = static_cast<const uint16_t*>(router_w);
+    p.bias = plan->bias;
+    p.w13 = static_cast<const uint8_t*>(w13);
+    p.w13s = w13_scale;
+    p.w2 = static_cast<const uint8_t*>(w2);
+    p.w2s = w2_scale;
+    p.out = static_cast<uint16_t*>(out);
+    p.ctl = plan->ctl;
+    p.logits = plan->logits;
+    p.xq = plan->xq;
+    p.xs = plan->xs;
+    p.act = plan->act;
+    p.out_acc = plan->out_acc;
+    p.spin_limit = kDefaultSpinTicks;
+    if (dbg) {
+        if ((dbg->topk_ids == nullptr) != (dbg->topk_w == nullptr)) return MONOMOE_ERR_INVALID;
+        if ((dbg->xq == nullptr) != (dbg->xs == nullptr)) return MONOMOE_ERR_INVALID;
+        if ((dbg->aq == nullptr) != (dbg->as == nullptr)) return MONOMOE_ERR_INVALID;
+        if ((dbg->topk_ids_in == nullptr) != (dbg->topk_w_in == nullptr)) return MONOMOE_ERR_INVALID;
+        p.d_ids = dbg->topk_ids;
+        p.d_w = dbg->topk_w;
+        p.d_xq = dbg->xq;
+        p.d_xs = dbg->xs;
+        p.d_act = dbg->act;
+        p.d_aq = dbg->aq;
+        p.d_as = dbg->as;
+        p.d_out = dbg->out_f32;
+        p.inj_ids = dbg->topk_ids_in;
+        p.inj_w = dbg->topk_w_in;
+        if (dbg->spin_limit_ticks) p.spin_limit = dbg->spin_limit_ticks;
+        p.fail_flag = dbg->fail_flag;
+    }
+    p.T = s.T;
+    p.E = s.E;
+    p.k = plan->topk;
+    p.renorm = plan->renorm;
+    p.lds_region = plan->lds_dyn;
+
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess || cur != plan->device) return MONOMOE_ERR_INVALID;
+    plan->kern->launch(p, plan->grid, (size_t)plan->lds_dyn, stream);
+    if (hipGetLastError() != hipSuccess) return MONOMOE_ERR_HIP;
+    return MONOMOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int monomoe_supported_shape(int32_t H, int32_t I) { return find_kernel(H, I) ? 1 : 0; }
+
+const char* monomoe_status_string(int status) {
+    switch (status) {
+        case MONOMOE_OK: return "ok";
+        case MONOMOE_ERR_INVALID: return "invalid argument";
+        case MONOMOE_ERR_UNSUPPORTED: return "unsupported shape";
+        case MONOMOE_ERR_OCCUPANCY: return "persistent grid cannot be resident";
+        case MONOMOE_ERR_HIP: return "HIP runtime error";
+        case MONOMOE_ERR_TIMEOUT: return "device readiness wait timed out";
+        default: return "unknown status";
+    }
+}
+
+int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_plan_t* plan_out) {
+    if (!shape || !plan_out) return MONOMOE_ERR_INVALID;
+    const monomoe_shape_t s = *shape;
+    if (s.T < 0 || s.H <= 0 || s.I <= 0 || s.E <= 0) return MONOMOE_ERR_INVALID;
+    if (s.H % 128 || s.I % 128) return MONOMOE_ERR_INVALID;
+    if (topk < 1 || topk > s.E) return MONOMOE_ERR_INVALID;
+    if (s.T > kTMax || s.E > kEMax || topk > kKMax) return MONOMOE_ERR_UNSUPPORTED;
+    const KernelEntry* kern = find_kernel(s.H, s.I);
+    if (!kern) return MONOMOE_ERR_UNSUPPORTED;
+
+    monomoe_plan_s* pl = new (std::nothrow) monomoe_plan_s();
+    if (!pl) return MONOMOE_ERR_HIP;
+    pl->shape = s;
+    pl->topk = topk;
+    pl->renorm = renorm ? 1 : 0;
+    pl->kern = kern;
+    pl->bias = nullptr;
+
+    int dev = 0;
+    hipDeviceProp_t prop;
+    if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+        delete pl;
+        return MONOMOE_ERR_HIP;
+    }
+    pl->device = dev;
+    pl->num_cus = prop.multiProcessorCount;
+    pl->lds_dyn = lds_region_bytes(s.H, s.I, s.T > 0 ? s.T : 1);
+
+    hipFuncAttributes attr;
+    if (hipFuncGetAttributes(&attr, kern->fn) != hipSuccess) {
+        delete pl;
+        return MONOMOE_ERR_HIP;
+    }
+    pl->lds_static = (int)attr.sharedSizeBytes;
+    if (pl->lds_dyn + pl->lds_static > (int)prop.sharedMemPerBlock) {
+        delete pl;
+        return MONOMOE_ERR_UNSUPPORTED;
+    }
+    if (hipFuncSetAttribute(kern->fn, hipFuncAttributeMaxDynamicSharedMemorySize, pl->lds_dyn) != hipSuccess) {
+        delete pl;
+        return MONOMOE_ERR_HIP;
+    }
+    int occ = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern->fn, kThreads, (size_t)pl->lds_dyn) != hipSuccess) {
+        delete pl;
+        return MONOMOE_ERR_HIP;
+    }
+    pl->occupancy = occ;
+    if (occ < 1) {
+        delete pl;
+        return MONOMOE_ERR_OCCUPANCY;
+    }
+    pl->grid = pl->num_cus;   // one resident workgroup per CU
+
+    // workspace: control words | logits | xq | xs | act | out_acc
+    const int T = s.T > 0 ? s.T : 1;
+    size_t off = 0;
+    const size_t o_ctl = off;    off = align_up(off + sizeof(uint32_t) * kCtlWords(s.H), 256);
+    const size_t o_log = off;    off = align_up(off + sizeof(float) * (size_t)T * s.E, 256);
+    const size_t o_xq = off;     off = align_up(off + (size_t)T * s.H, 256);
+    const size_t o_xs = off;     off = align_up(off + sizeof(float) * (size_t)T * (s.H / 128), 256);
+    const size_t o_act = off;    off = align_up(off + sizeof(float) * (size_t)T * topk * s.I, 256);
+    const size_t o_out = off;    off = align_up(off + sizeof(float) * (size_t)T * s.H, 256);
+    pl->ws_bytes = off;
+    if (hipMalloc(&pl->ws, pl->ws_bytes) != hipSuccess) {
+        delete pl;
+        return MONOMOE_ERR_HIP;
+    }
+    uint8_t* base = static_cast<uint8_t*>(pl->ws);
+    pl->ctl = reinterpret_cast<uint32_t*>(base + o_ctl);
+    pl->logits = reinterpret_cast<float*>(base + o_log);
+    pl->xq = base + o_xq;
+    pl->xs = reinterpret_cast<float*>(base + o_xs);
+    pl->act = reinterpret_cast<float*>(base + o_act);
+    pl->out_acc = reinterpret_cast<float*>(base + o_out);
+    const int zr = zero_workspace(pl);
+    if (zr != MONOMOE_OK) {
+        (void)hipFree(pl->ws);
+        delete pl;
+        return zr;
+    }
+    *plan_out = pl;
+    return MONOMOE_OK;
+}
+
+void monomoe_plan_destroy(monomoe_plan_t plan) {
+    if (!plan) return;
+    if (plan->ws) (void)hipFree(plan->ws);
+    delete plan;
+}
+
+int monomoe_plan_set_router_bias(monomoe_plan_t plan, const float* bias) {
+    if (!plan) return MONOMOE_ERR_INVALID;
+    if (bias && !aligned16(bias)) return MONOMOE_ERR_INVALID;
+    plan->bias = bias;
+    return MONOMOE_OK;
+}
+
+int monomoe_forward(monomoe_plan_t plan, const void* x, const void* router_w, const void* w13,
+                    const float* w13_scale, const void* w2, const float* w2_scale, void* out, hipStream_t stream) {
+    return launch(plan, x, router_w, w13, w13_scale, w2, w2_scale, out, nullptr, stream);
+}
+
+int monomoe_forward_debug(monomoe_plan_t plan, const void* x, const void* router_w, const void* w13,
+                          const float* w13_scale, const void* w2, const float* w2_scale, void* out,
+                          const monomoe_debug_t* dbg, hipStream_t stream) {
+    return launch(plan, x, router_w, w13, w13_scale, w2, w2_scale, out, dbg, stream);
+}
+
+int monomoe_plan_status(monomoe_plan_t plan) {
+    if (!plan) return MONOMOE_ERR_INVALID;
+    if (hipDeviceSynchronize() != hipSuccess) return MONOMOE_ERR_HIP;
+    uint32_t st = 0;
+    if (hipMemcpy(&st, plan->ctl + kCtlStatus, sizeof st, hipMemcpyDeviceToHost) != hipSuccess) return MONOMOE_ERR_HIP;
+    if (st == kDevOk) return MONOMOE_OK;
+    if (st == kDevTimeout) return MONOMOE_ERR_TIMEOUT;
+    return MONOMOE_ERR_INVALID;
+}
+
+int monomoe_plan_reset(monomoe_plan_t plan) {
+    if (!plan) return MONOMOE_ERR_INVALID;
+    if (hipDeviceSynchronize() != hipSuccess) return MONOMOE_ERR_HIP;
+    return zero_workspace(plan);
+}
+
+int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info) {
+    if (!plan || !info) return MONOMOE_ERR_INVALID;
+    info->grid = plan->grid;
+    info->block = kThreads;
+    info->lds_bytes = plan->lds_dyn + plan->lds_static;
+    info->occupancy = plan->occupancy;
+    info->num_cus = plan->num_cus;
+    info->workspace_bytes = (int64_t)plan->ws_bytes;
+    return MONOMOE_OK;
+}
+
+}  // extern "C"

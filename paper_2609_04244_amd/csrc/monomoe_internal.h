@@ -1,0 +1,98 @@
+// Internal interface between the host runtime (monomoe_api.hip) and the persistent
+// kernel (monomoe_kernel.hip).  Not installed; not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace monomoe {
+
+constexpr int kComputeWaves = 4;              // wavefronts that stream weights and run MFMAs
+constexpr int kWaves = kComputeWaves + 1;     // + one helper wavefront (epilogues, flags)
+constexpr int kThreads = kWaves * 64;
+constexpr int kTMax = 16;                     // tokens per step: one 16-wide MFMA N tile
+constexpr int kKMax = 16;                     // top-k bound
+constexpr int kEMax = 512;                    // experts bound (8 logits per lane in top-k)
+constexpr int kUMax = kTMax * kKMax;          // active experts bound (T*k, also <= E)
+constexpr int kSlots = 4;                     // partial-sum hand-off slots per workgroup
+constexpr int kXcds = 8;                      // XCDs; workgroups are dealt round-robin
+
+// Control words at the head of the workspace (uint32 each).  Every counter is zero
+// when no launch is in flight: the last user of each counter clears it, and the last
+// workgroup to leave a launch clears the rest.
+enum : int {
+    kCtlRoute = 0,              // XCDs whose workgroups all published routing inputs
+    kCtlExit = 1,               // workgroups that finished the launch
+    kCtlStatus = 2,             // sticky device status (kDev*)
+    kCtlRouteXcd = 8,           // [kXcds] workgroups of each XCD that published
+    kCtlUp = 16,                // [kUMax] requantised 128-groups per active-expert slot
+    kCtlTile = kCtlUp + kUMax,  // [H/16] finished down units per 16-row output tile
+};
+// then [kUMax * I/128] gate/up units finished per (active-expert slot, 128-group)
+constexpr int ctl_grp_offset(int H) { return kCtlTile + H / 16; }
+constexpr int ctl_words(int H, int I) { return ctl_grp_offset(H) + kUMax * (I / 128); }
+
+enum : uint32_t { kDevOk = 0, kDevTimeout = 1, kDevBadIds = 2 };
+
+struct KParams {
+    // operator inputs/outputs (caller-owned)
+    const uint16_t* x;        // bf16 [T,H]
+    const uint16_t* rw;       // bf16 [E,H]
+    const float* bias;        // fp32 [E] or null
+    const uint8_t* w13;       // e4m3 [E,2I,H]
+    const float* w13s;        // fp32 [E,2I/128,H/128]
+    const uint8_t* w2;        // e4m3 [E,H,I]
+    const float* w2s;         // fp32 [E,H/128,I/128]
+    uint16_t* out;            // bf16 [T,H]
+    // plan workspace
+    uint32_t* ctl;            // control words
+    float* logits;            // [T,E]
+    uint8_t* xq;              // [T,H]      quantised input
+    float* xs;                // [T,H/128]  input group scales
+    float* act;               // [T*k,I]    SiLU(gate)*up
+    uint8_t* aq;              // [T*k,I]    requantised act
+    float* as;                // [T*k,I/128]
+    float* out_acc;           // [T,H]      fp32 accumulator, zero between launches
+    // test hooks (null when unused)
+    int32_t* d_ids;
+    float* d_w;
+    uint8_t* d_xq;
+    float* d_xs;
+    float* d_act;
+    uint8_t* d_aq;
+    float* d_as;
+    float* d_out;
+    const int32_t* inj_ids;
+    const float* inj_w;
+    uint64_t spin_limit;      // 100 MHz ticks
+    int32_t fail_flag;
+    // runtime shape and LDS layout
+    int32_t T, E, k, renorm;
+    int32_t naq;              // requantised-act LDS buffers (2 = double buffered, 1)
+};
+
+// One compiled (H, I) specialisation.
+struct KernelEntry {
+    int H, I;
+    const void* fn;                                          // __global__ symbol
+    void (*launch)(const KParams&, int grid, size_t lds, hipStream_t);
+};
+
+const KernelEntry* find_kernel(int H, int I);
+int kernel_count();
+const KernelEntry* kernel_at(int i);
+
+// Dynamic LDS: the phase-aliased region (quantised input during gate/up; `naq`
+// requantised-act buffers during down) followed by the partial-sum hand-off slots.
+inline int lds_region_bytes(int H, int I, int T, int naq) {
+    const int up = T * (H + 16) + T * (H / 128) * 4;
+    const int dn = naq * (T * (I + 16) + T * (I / 128) * 4);
+    const int m = up > dn ? up : dn;
+    return (m + 15) & ~15;
+}
+inline int lds_partials_bytes() { return kSlots * kComputeWaves * 64 * 16; }
+inline int lds_dynamic_bytes(int H, int I, int T, int naq) {
+    return lds_region_bytes(H, I, T, naq) + lds_partials_bytes();
+}
+
+}  // namespace monomoe

@@ -1,0 +1,214 @@
+"""Thin ctypes binding of ``libmonomoe.so`` (the C ABI declared in include/monomoe.h).
+
+Argument marshalling only: tensors are passed as device pointers and the current torch
+stream as the ``hipStream_t``; every step of the operator runs in the HIP kernel.  There
+is no fallback: if the library is missing this module raises.
+"""
+import ctypes
+import os
+
+import torch  # loads torch's HIP runtime first, so the library binds to the same one
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmonomoe.so")
+
+MONOMOE_OK = 0
+MONOMOE_ERR_INVALID = -1
+MONOMOE_ERR_UNSUPPORTED = -2
+MONOMOE_ERR_OCCUPANCY = -3
+MONOMOE_ERR_HIP = -4
+MONOMOE_ERR_TIMEOUT = -5
+
+# Every symbol include/monomoe.h declares.
+EXPORTS = (
+    "monomoe_plan", "monomoe_plan_destroy", "monomoe_plan_set_router_bias", "monomoe_forward",
+    "monomoe_forward_debug", "monomoe_plan_status", "monomoe_plan_reset", "monomoe_plan_info",
+    "monomoe_supported_shape", "monomoe_status_string",
+)
+
+
+class MonoMoEError(RuntimeError):
+    def __init__(self, code, what):
+        self.code = code
+        super().__init__("%s failed: %s (%d)" % (what, status_string(code), code))
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("H", ctypes.c_int32), ("E", ctypes.c_int32), ("I", ctypes.c_int32)]
+
+
+class Debug(ctypes.Structure):
+    _fields_ = [
+        ("topk_ids", ctypes.c_void_p), ("topk_w", ctypes.c_void_p), ("xq", ctypes.c_void_p),
+        ("xs", ctypes.c_void_p), ("act", ctypes.c_void_p), ("aq", ctypes.c_void_p), ("as_", ctypes.c_void_p),
+        ("out_f32", ctypes.c_void_p), ("topk_ids_in", ctypes.c_void_p), ("topk_w_in", ctypes.c_void_p),
+        ("spin_limit_ticks", ctypes.c_uint64), ("fail_flag", ctypes.c_int32),
+    ]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("grid", ctypes.c_int32), ("block", ctypes.c_int32), ("lds_bytes", ctypes.c_int32),
+                ("occupancy", ctypes.c_int32), ("num_cus", ctypes.c_int32), ("workspace_bytes", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libmonomoe.so (built by __graft_entry__.build()); raise if it is missing."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libmonomoe.so is not built (%s); run __graft_entry__.build()" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        vp = ctypes.c_void_p
+        L.monomoe_plan.argtypes = [ctypes.POINTER(Shape), ctypes.c_int, ctypes.c_int, ctypes.POINTER(vp)]
+        L.monomoe_plan.restype = ctypes.c_int
+        L.monomoe_plan_destroy.argtypes = [vp]
+        L.monomoe_plan_destroy.restype = None
+        L.monomoe_plan_set_router_bias.argtypes = [vp, vp]
+        L.monomoe_plan_set_router_bias.restype = ctypes.c_int
+        L.monomoe_forward.argtypes = [vp] * 9
+        L.monomoe_forward.restype = ctypes.c_int
+        L.monomoe_forward_debug.argtypes = [vp] * 8 + [ctypes.POINTER(Debug), vp]
+        L.monomoe_forward_debug.restype = ctypes.c_int
+        L.monomoe_plan_status.argtypes = [vp]
+        L.monomoe_plan_status.restype = ctypes.c_int
+        L.monomoe_plan_reset.argtypes = [vp]
+        L.monomoe_plan_reset.restype = ctypes.c_int
+        L.monomoe_plan_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]
+        L.monomoe_plan_info.restype = ctypes.c_int
+        L.monomoe_supported_shape.argtypes = [ctypes.c_int32, ctypes.c_int32]
+        L.monomoe_supported_shape.restype = ctypes.c_int
+        L.monomoe_status_string.argtypes = [ctypes.c_int]
+        L.monomoe_status_string.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def status_string(code):
+    return lib().monomoe_status_string(int(code)).decode()
+
+
+def supported_shape(H, I):
+    return bool(lib().monomoe_supported_shape(int(H), int(I)))
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Plan:
+    """A plan for one shape (T, H, E, I) with top-k and renormalisation fixed."""
+
+    def __init__(self, T, H, E, I, topk, renorm=True):
+        self.T, self.H, self.E, self.I, self.topk, self.renorm = int(T), int(H), int(E), int(I), int(topk), bool(renorm)
+        self._h = ctypes.c_void_p()
+        self._bias = None
+        rc = lib().monomoe_plan(ctypes.byref(Shape(self.T, self.H, self.E, self.I)), self.topk, int(self.renorm),
+                                ctypes.byref(self._h))
+        if rc != MONOMOE_OK:
+            raise MonoMoEError(rc, "monomoe_plan")
+
+    def close(self):
+        if self._h:
+            lib().monomoe_plan_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def set_router_bias(self, bias):
+        self._bias = bias  # keep the tensor alive while the plan refers to it
+        rc = lib().monomoe_plan_set_router_bias(self._h, _ptr(bias))
+        if rc != MONOMOE_OK:
+            raise MonoMoEError(rc, "monomoe_plan_set_router_bias")
+
+    def info(self):
+        inf = PlanInfo()
+        rc = lib().monomoe_plan_info(self._h, ctypes.byref(inf))
+        if rc != MONOMOE_OK:
+            raise MonoMoEError(rc, "monomoe_plan_info")
+        return {f: getattr(inf, f) for f, _ in PlanInfo._fields_}
+
+    def _check(self, x, router_w, w13, w13_scale, w2, w2_scale, out):
+        T, H, E, I = self.T, self.H, self.E, self.I
+        want = [
+            (x, (T, H), torch.bfloat16), (router_w, (E, H), torch.bfloat16),
+            (w13, (E, 2 * I, H), torch.uint8), (w13_scale, (E, 2 * I // 128, H // 128), torch.float32),
+            (w2, (E, H, I), torch.uint8), (w2_scale, (E, H // 128, I // 128), torch.float32),
+            (out, (T, H), torch.bfloat16),
+        ]
+        for t, shape, dtype in want:
+            if tuple(t.shape) != shape or t.dtype != dtype or not t.is_contiguous() or not t.is_cuda:
+                raise ValueError("expected a contiguous device tensor %s of %s, got %s %s"
+                                 % (shape, dtype, tuple(t.shape), t.dtype))
+
+    def forward(self, x, router_w, w13, w13_scale, w2, w2_scale, out=None, stream=None, check=True):
+        """Enqueue the fused operator; returns out (bf16 [T,H])."""
+        if out is None:
+            out = torch.empty((self.T, self.H), dtype=torch.bfloat16, device=x.device)
+        if check:
+            self._check(x, router_w, w13, w13_scale, w2, w2_scale, out)
+        rc = lib().monomoe_forward(self._h, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale), _ptr(w2),
+                                   _ptr(w2_scale), _ptr(out), _stream(stream))
+        if rc != MONOMOE_OK:
+            raise MonoMoEError(rc, "monomoe_forward")
+        return out
+
+    def forward_debug(self, x, router_w, w13, w13_scale, w2, w2_scale, out=None, ids_in=None, w_in=None,
+                      spin_limit_ticks=0, fail_flag=False, stream=None):
+        """Forward with every test hook enabled; returns (out, dict of device tensors)."""
+        T, H, I, k = self.T, self.H, self.I, self.topk
+        dev = x.device
+        if out is None:
+            out = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+        self._check(x, router_w, w13, w13_scale, w2, w2_scale, out)
+        d = {
+            "ids": torch.full((T, k), -1, dtype=torch.int32, device=dev),
+            "w": torch.zeros((T, k), dtype=torch.float32, device=dev),
+            "xq": torch.zeros((T, H), dtype=torch.uint8, device=dev),
+            "xs": torch.zeros((T, H // 128), dtype=torch.float32, device=dev),
+            "act": torch.zeros((T * k, I), dtype=torch.float32, device=dev),
+            "aq": torch.zeros((T * k, I), dtype=torch.uint8, device=dev),
+            "as": torch.zeros((T * k, I // 128), dtype=torch.float32, device=dev),
+            "out_f32": torch.zeros((T, H), dtype=torch.float32, device=dev),
+        }
+        if (ids_in is None) != (w_in is None):
+            raise ValueError("ids_in and w_in go together")
+        if ids_in is not None:
+            ids_in = ids_in.to(device=dev, dtype=torch.int32).contiguous()
+            w_in = w_in.to(device=dev, dtype=torch.float32).contiguous()
+        dbg = Debug(d["ids"].data_ptr(), d["w"].data_ptr(), d["xq"].data_ptr(), d["xs"].data_ptr(),
+                    d["act"].data_ptr(), d["aq"].data_ptr(), d["as"].data_ptr(), d["out_f32"].data_ptr(),
+                    ids_in.data_ptr() if ids_in is not None else None,
+                    w_in.data_ptr() if w_in is not None else None,
+                    int(spin_limit_ticks), int(bool(fail_flag)))
+        rc = lib().monomoe_forward_debug(self._h, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale), _ptr(w2),
+                                         _ptr(w2_scale), _ptr(out), ctypes.byref(dbg), _stream(stream))
+        if rc != MONOMOE_OK:
+            raise MonoMoEError(rc, "monomoe_forward_debug")
+        d["_keep"] = (ids_in, w_in)
+        return out, d
+
+    def status(self):
+        return lib().monomoe_plan_status(self._h)
+
+    def reset(self):
+        rc = lib().monomoe_plan_reset(self._h)
+        if rc != MONOMOE_OK:
+            raise MonoMoEError(rc, "monomoe_plan_reset")
