@@ -19,6 +19,7 @@ struct monomoe_plan_s {
     int grid;
     int lds_dyn;
     int lds_static;
+    int naq;
     const float* bias;
     // workspace (one allocation)
     void* ws;
@@ -28,6 +29,8 @@ struct monomoe_plan_s {
     uint8_t* xq;
     float* xs;
     float* act;
+    uint8_t* aq;
+    float* as;
     float* out_acc;
 };
 
@@ -70,6 +73,8 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
     p.xq = plan->xq;
     p.xs = plan->xs;
     p.act = plan->act;
+    p.aq = plan->aq;
+    p.as = plan->as;
     p.out_acc = plan->out_acc;
     p.spin_limit = kDefaultSpinTicks;
     if (dbg) {
@@ -94,7 +99,7 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
     p.E = s.E;
     p.k = plan->topk;
     p.renorm = plan->renorm;
-    p.lds_region = plan->lds_dyn;
+    p.naq = plan->naq;
 
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess || cur != plan->device) return MONOMOE_ERR_INVALID;
@@ -147,15 +152,18 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     }
     pl->device = dev;
     pl->num_cus = prop.multiProcessorCount;
-    pl->lds_dyn = lds_region_bytes(s.H, s.I, s.T > 0 ? s.T : 1);
-
     hipFuncAttributes attr;
     if (hipFuncGetAttributes(&attr, kern->fn) != hipSuccess) {
         delete pl;
         return MONOMOE_ERR_HIP;
     }
     pl->lds_static = (int)attr.sharedSizeBytes;
-    if (pl->lds_dyn + pl->lds_static > (int)prop.sharedMemPerBlock) {
+    // double-buffer the requantised activation in LDS when it fits, else single-buffer
+    const int Tl = s.T > 0 ? s.T : 1;
+    const int lds_cap = (int)prop.sharedMemPerBlock - pl->lds_static;
+    pl->naq = lds_dynamic_bytes(s.H, s.I, Tl, 2) <= lds_cap ? 2 : 1;
+    pl->lds_dyn = lds_dynamic_bytes(s.H, s.I, Tl, pl->naq);
+    if (pl->lds_dyn > lds_cap) {
         delete pl;
         return MONOMOE_ERR_UNSUPPORTED;
     }
@@ -175,14 +183,16 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     }
     pl->grid = pl->num_cus;   // one resident workgroup per CU
 
-    // workspace: control words | logits | xq | xs | act | out_acc
-    const int T = s.T > 0 ? s.T : 1;
+    // workspace: control words | logits | xq | xs | act | aq | as | out_acc
+    const int T = Tl;
     size_t off = 0;
-    const size_t o_ctl = off;    off = align_up(off + sizeof(uint32_t) * kCtlWords(s.H), 256);
+    const size_t o_ctl = off;    off = align_up(off + sizeof(uint32_t) * ctl_words(s.H, s.I), 256);
     const size_t o_log = off;    off = align_up(off + sizeof(float) * (size_t)T * s.E, 256);
     const size_t o_xq = off;     off = align_up(off + (size_t)T * s.H, 256);
     const size_t o_xs = off;     off = align_up(off + sizeof(float) * (size_t)T * (s.H / 128), 256);
     const size_t o_act = off;    off = align_up(off + sizeof(float) * (size_t)T * topk * s.I, 256);
+    const size_t o_aq = off;     off = align_up(off + (size_t)T * topk * s.I, 256);
+    const size_t o_as = off;     off = align_up(off + sizeof(float) * (size_t)T * topk * (s.I / 128), 256);
     const size_t o_out = off;    off = align_up(off + sizeof(float) * (size_t)T * s.H, 256);
     pl->ws_bytes = off;
     if (hipMalloc(&pl->ws, pl->ws_bytes) != hipSuccess) {
@@ -195,6 +205,8 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     pl->xq = base + o_xq;
     pl->xs = reinterpret_cast<float*>(base + o_xs);
     pl->act = reinterpret_cast<float*>(base + o_act);
+    pl->aq = base + o_aq;
+    pl->as = reinterpret_cast<float*>(base + o_as);
     pl->out_acc = reinterpret_cast<float*>(base + o_out);
     const int zr = zero_workspace(pl);
     if (zr != MONOMOE_OK) {

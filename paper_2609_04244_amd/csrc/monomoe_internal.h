@@ -84,14 +84,19 @@ const KernelEntry* kernel_at(int i);
 
 // Dynamic LDS: the phase-aliased region (quantised input during gate/up; `naq`
 // requantised-act buffers during down) followed by the partial-sum hand-off slots.
-inline int lds_region_bytes(int H, int I, int T, int naq) {
-    const int up = T * (H + 16) + T * (H / 128) * 4;
-    const int dn = naq * (T * (I + 16) + T * (I / 128) * 4);
+// Rows are padded by 16 bytes; every buffer starts 16-byte aligned.
+__host__ __device__ inline int lds_up_bytes(int H, int T) { return T * (H + 16) + T * (H / 128) * 4; }
+__host__ __device__ inline int lds_aq_buffer_bytes(int I, int T) {
+    return (T * (I + 16) + T * (I / 128) * 4 + 15) & ~15;
+}
+__host__ __device__ inline int lds_region_bytes(int H, int I, int T, int naq) {
+    const int up = lds_up_bytes(H, T);
+    const int dn = naq * lds_aq_buffer_bytes(I, T);
     const int m = up > dn ? up : dn;
     return (m + 15) & ~15;
 }
-inline int lds_partials_bytes() { return kSlots * kComputeWaves * 64 * 16; }
-inline int lds_dynamic_bytes(int H, int I, int T, int naq) {
+__host__ __device__ inline int lds_partials_bytes() { return kSlots * kComputeWaves * 64 * 16; }
+__host__ __device__ inline int lds_dynamic_bytes(int H, int I, int T, int naq) {
     return lds_region_bytes(H, I, T, naq) + lds_partials_bytes();
 }
 
