@@ -99,6 +99,8 @@ int monomoe_forward(monomoe_plan_t plan, const void* x, const void* router_w,
  *   out_f32   fp32  [T,H]         the weighted sum before rounding to bf16 (written)
  *   topk_ids_in / topk_w_in       [T,topk] replace the kernel's own selection (read);
  *                                 both or neither; ids distinct per token, in [0,E)
+ *   stamps    u64   [grid,16]     per-workgroup s_memrealtime (100 MHz) stamps at phase
+ *                                 boundaries, for latency breakdowns (written)
  *   spin_limit_ticks              bound of every readiness wait in 100 MHz ticks
  *                                 (0 = the default of 2 s)
  *   fail_flag                     nonzero makes the routing wait target unreachable, so
@@ -115,6 +117,7 @@ typedef struct {
     float* out_f32;
     const int32_t* topk_ids_in;
     const float* topk_w_in;
+    uint64_t* stamps;
     uint64_t spin_limit_ticks;
     int32_t fail_flag;
 } monomoe_debug_t;
@@ -150,6 +153,18 @@ int monomoe_supported_shape(int32_t H, int32_t I);
 
 /* Static string for a status code. */
 const char* monomoe_status_string(int status);
+
+/* Measurement references (not part of the operator).  Plain dwordx4 grid-stride kernels
+ * enqueued on `stream`:
+ *   monomoe_stream_copy: dst[0,bytes) = src[0,bytes); a kernel of exactly known HBM
+ *     traffic (bytes read + bytes written), used to calibrate HBM byte counters.
+ *   monomoe_stream_read: reads src[0,bytes); the achievable streaming-read bandwidth,
+ *     reported next to the nominal peak.  sink16 is a 16-byte device scratch word that
+ *     is written only in a practically impossible case (it keeps the loads alive).
+ * Pointers are device pointers, 16-byte aligned; bytes a multiple of 16.
+ * MONOMOE_ERR_INVALID otherwise, MONOMOE_ERR_HIP if the launch fails. */
+int monomoe_stream_copy(void* dst, const void* src, size_t bytes, hipStream_t stream);
+int monomoe_stream_read(const void* src, size_t bytes, void* sink16, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -10,7 +10,7 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmonomoe.so")
-SOURCES = ["monomoe_kernel.hip", "monomoe_api.hip"]
+SOURCES = ["monomoe_kernel.hip", "monomoe_api.hip", "monomoe_stream.hip"]
 ARCH = "gfx950"
 
 
@@ -23,13 +23,28 @@ def command():
             "-o", LIB] + [os.path.join(CSRC, s) for s in SOURCES]
 
 
-def build(verbose=False):
-    cmd = command()
+PROFILER = os.path.join(HERE, "monomoe_profile")
+
+
+def profiler_command():
+    hipcc = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "bin", "hipcc")
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    return [hipcc, "--offload-arch=" + ARCH, "-O2", "-std=c++17", "-Wno-unused-command-line-argument",
+            os.path.join(CSRC, "monomoe_profile.cpp"), "-L" + HERE, "-l:libmonomoe.so",
+            "-L" + os.path.join(rocm, "lib"), "-lamdhip64", "-Wl,-rpath,$ORIGIN", "-o", PROFILER]
+
+
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     if res.returncode != 0:
         raise RuntimeError("hipcc failed:\n" + res.stdout)
+
+
+def build(verbose=False):
+    _run(command(), verbose)
+    _run(profiler_command(), verbose)
     return LIB
 
 

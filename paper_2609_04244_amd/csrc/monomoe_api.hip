@@ -92,6 +92,7 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
         p.d_out = dbg->out_f32;
         p.inj_ids = dbg->topk_ids_in;
         p.inj_w = dbg->topk_w_in;
+        p.stamps = dbg->stamps;
         if (dbg->spin_limit_ticks) p.spin_limit = dbg->spin_limit_ticks;
         p.fail_flag = dbg->fail_flag;
     }

@@ -34,6 +34,13 @@ constexpr int ctl_words(int H, int I) { return ctl_grp_offset(H) + kUMax * (I / 
 
 enum : uint32_t { kDevOk = 0, kDevTimeout = 1, kDevBadIds = 2 };
 
+// Phase stamps (test hook): per workgroup, s_memrealtime at these points.
+constexpr int kStamps = 16;
+enum : int {
+    kStEntry = 0, kStPublished, kStRouted, kStMeta, kStXqStaged, kStUpDone, kStFirstAq, kStDownDone,
+    kStExit, kStFirstMfma, kStComputeDone, kStRouter, kStQuant, kStTopk,
+};
+
 struct KParams {
     // operator inputs/outputs (caller-owned)
     const uint16_t* x;        // bf16 [T,H]
@@ -64,6 +71,7 @@ struct KParams {
     float* d_out;
     const int32_t* inj_ids;
     const float* inj_w;
+    uint64_t* stamps;         // [grid][kStamps]
     uint64_t spin_limit;      // 100 MHz ticks
     int32_t fail_flag;
     // runtime shape and LDS layout

@@ -23,7 +23,7 @@ MONOMOE_ERR_TIMEOUT = -5
 EXPORTS = (
     "monomoe_plan", "monomoe_plan_destroy", "monomoe_plan_set_router_bias", "monomoe_forward",
     "monomoe_forward_debug", "monomoe_plan_status", "monomoe_plan_reset", "monomoe_plan_info",
-    "monomoe_supported_shape", "monomoe_status_string",
+    "monomoe_supported_shape", "monomoe_status_string", "monomoe_stream_copy", "monomoe_stream_read",
 )
 
 
@@ -42,7 +42,7 @@ class Debug(ctypes.Structure):
         ("topk_ids", ctypes.c_void_p), ("topk_w", ctypes.c_void_p), ("xq", ctypes.c_void_p),
         ("xs", ctypes.c_void_p), ("act", ctypes.c_void_p), ("aq", ctypes.c_void_p), ("as_", ctypes.c_void_p),
         ("out_f32", ctypes.c_void_p), ("topk_ids_in", ctypes.c_void_p), ("topk_w_in", ctypes.c_void_p),
-        ("spin_limit_ticks", ctypes.c_uint64), ("fail_flag", ctypes.c_int32),
+        ("stamps", ctypes.c_void_p), ("spin_limit_ticks", ctypes.c_uint64), ("fail_flag", ctypes.c_int32),
     ]
 
 
@@ -82,6 +82,10 @@ def lib():
         L.monomoe_supported_shape.restype = ctypes.c_int
         L.monomoe_status_string.argtypes = [ctypes.c_int]
         L.monomoe_status_string.restype = ctypes.c_char_p
+        L.monomoe_stream_copy.argtypes = [vp, vp, ctypes.c_size_t, vp]
+        L.monomoe_stream_copy.restype = ctypes.c_int
+        L.monomoe_stream_read.argtypes = [vp, ctypes.c_size_t, vp, vp]
+        L.monomoe_stream_read.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -92,6 +96,22 @@ def status_string(code):
 
 def supported_shape(H, I):
     return bool(lib().monomoe_supported_shape(int(H), int(I)))
+
+
+def stream_copy(dst, src, nbytes=None, stream=None):
+    """Reference copy kernel: dst[:nbytes] = src[:nbytes] (device tensors)."""
+    n = int(src.numel() * src.element_size() if nbytes is None else nbytes)
+    rc = lib().monomoe_stream_copy(ctypes.c_void_p(dst.data_ptr()), ctypes.c_void_p(src.data_ptr()), n, _stream(stream))
+    if rc != MONOMOE_OK:
+        raise MonoMoEError(rc, "monomoe_stream_copy")
+
+
+def stream_read(src, sink, nbytes=None, stream=None):
+    """Reference read-only streaming kernel over src[:nbytes]; sink is a 16-byte device tensor."""
+    n = int(src.numel() * src.element_size() if nbytes is None else nbytes)
+    rc = lib().monomoe_stream_read(ctypes.c_void_p(src.data_ptr()), n, ctypes.c_void_p(sink.data_ptr()), _stream(stream))
+    if rc != MONOMOE_OK:
+        raise MonoMoEError(rc, "monomoe_stream_read")
 
 
 def _ptr(t):
@@ -187,6 +207,7 @@ class Plan:
             "aq": torch.zeros((T * k, I), dtype=torch.uint8, device=dev),
             "as": torch.zeros((T * k, I // 128), dtype=torch.float32, device=dev),
             "out_f32": torch.zeros((T, H), dtype=torch.float32, device=dev),
+            "stamps": torch.zeros((self.info()["grid"], 16), dtype=torch.int64, device=dev),
         }
         if (ids_in is None) != (w_in is None):
             raise ValueError("ids_in and w_in go together")
@@ -197,7 +218,7 @@ class Plan:
                     d["act"].data_ptr(), d["aq"].data_ptr(), d["as"].data_ptr(), d["out_f32"].data_ptr(),
                     ids_in.data_ptr() if ids_in is not None else None,
                     w_in.data_ptr() if w_in is not None else None,
-                    int(spin_limit_ticks), int(bool(fail_flag)))
+                    d["stamps"].data_ptr(), int(spin_limit_ticks), int(bool(fail_flag)))
         rc = lib().monomoe_forward_debug(self._h, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale), _ptr(w2),
                                          _ptr(w2_scale), _ptr(out), ctypes.byref(dbg), _stream(stream))
         if rc != MONOMOE_OK:
