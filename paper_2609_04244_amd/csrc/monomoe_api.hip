@@ -20,14 +20,13 @@ struct monomoe_plan_s {
     int lds_dyn;
     int lds_static;
     int naq;
+    int nslots;
     const float* bias;
     // workspace (one allocation)
     void* ws;
     size_t ws_bytes;
     uint32_t* ctl;
     float* logits;
-    uint8_t* xq;
-    float* xs;
     float* act;
     uint8_t* aq;
     float* as;
@@ -70,8 +69,6 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
     p.out = static_cast<uint16_t*>(out);
     p.ctl = plan->ctl;
     p.logits = plan->logits;
-    p.xq = plan->xq;
-    p.xs = plan->xs;
     p.act = plan->act;
     p.aq = plan->aq;
     p.as = plan->as;
@@ -101,6 +98,7 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
     p.k = plan->topk;
     p.renorm = plan->renorm;
     p.naq = plan->naq;
+    p.nslots = plan->nslots;
 
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess || cur != plan->device) return MONOMOE_ERR_INVALID;
@@ -159,11 +157,16 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
         return MONOMOE_ERR_HIP;
     }
     pl->lds_static = (int)attr.sharedSizeBytes;
-    // double-buffer the requantised activation in LDS when it fits, else single-buffer
+    // double-buffer the requantised activation in LDS when it fits, else single-buffer;
+    // then as many partial-sum slots as the rest of the LDS holds (more slots let the
+    // compute wavefronts run further ahead of the helper's epilogues)
     const int Tl = s.T > 0 ? s.T : 1;
     const int lds_cap = (int)prop.sharedMemPerBlock - pl->lds_static;
-    pl->naq = lds_dynamic_bytes(s.H, s.I, Tl, 2) <= lds_cap ? 2 : 1;
-    pl->lds_dyn = lds_dynamic_bytes(s.H, s.I, Tl, pl->naq);
+    pl->naq = lds_dynamic_bytes(s.H, s.I, Tl, 2, kSlotsMin) <= lds_cap ? 2 : 1;
+    pl->nslots = kSlotsMin;
+    while (pl->nslots < kSlotsMax && lds_dynamic_bytes(s.H, s.I, Tl, pl->naq, pl->nslots * 2) <= lds_cap)
+        pl->nslots *= 2;
+    pl->lds_dyn = lds_dynamic_bytes(s.H, s.I, Tl, pl->naq, pl->nslots);
     if (pl->lds_dyn > lds_cap) {
         delete pl;
         return MONOMOE_ERR_UNSUPPORTED;
@@ -184,13 +187,11 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     }
     pl->grid = pl->num_cus;   // one resident workgroup per CU
 
-    // workspace: control words | logits | xq | xs | act | aq | as | out_acc
+    // workspace: control words | logits | act | aq | as | out_acc
     const int T = Tl;
     size_t off = 0;
     const size_t o_ctl = off;    off = align_up(off + sizeof(uint32_t) * ctl_words(s.H, s.I), 256);
     const size_t o_log = off;    off = align_up(off + sizeof(float) * (size_t)T * s.E, 256);
-    const size_t o_xq = off;     off = align_up(off + (size_t)T * s.H, 256);
-    const size_t o_xs = off;     off = align_up(off + sizeof(float) * (size_t)T * (s.H / 128), 256);
     const size_t o_act = off;    off = align_up(off + sizeof(float) * (size_t)T * topk * s.I, 256);
     const size_t o_aq = off;     off = align_up(off + (size_t)T * topk * s.I, 256);
     const size_t o_as = off;     off = align_up(off + sizeof(float) * (size_t)T * topk * (s.I / 128), 256);
@@ -203,8 +204,6 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     uint8_t* base = static_cast<uint8_t*>(pl->ws);
     pl->ctl = reinterpret_cast<uint32_t*>(base + o_ctl);
     pl->logits = reinterpret_cast<float*>(base + o_log);
-    pl->xq = base + o_xq;
-    pl->xs = reinterpret_cast<float*>(base + o_xs);
     pl->act = reinterpret_cast<float*>(base + o_act);
     pl->aq = base + o_aq;
     pl->as = reinterpret_cast<float*>(base + o_as);

@@ -14,7 +14,8 @@ constexpr int kTMax = 16;                     // tokens per step: one 16-wide MF
 constexpr int kKMax = 16;                     // top-k bound
 constexpr int kEMax = 512;                    // experts bound (8 logits per lane in top-k)
 constexpr int kUMax = kTMax * kKMax;          // active experts bound (T*k, also <= E)
-constexpr int kSlots = 4;                     // partial-sum hand-off slots per workgroup
+constexpr int kSlotsMin = 4;                  // partial-sum hand-off slots per workgroup:
+constexpr int kSlotsMax = 32;                 //   a power of two in [min, max], as LDS allows
 constexpr int kXcds = 8;                      // XCDs; workgroups are dealt round-robin
 
 // Control words at the head of the workspace (uint32 each).  Every counter is zero
@@ -54,8 +55,6 @@ struct KParams {
     // plan workspace
     uint32_t* ctl;            // control words
     float* logits;            // [T,E]
-    uint8_t* xq;              // [T,H]      quantised input
-    float* xs;                // [T,H/128]  input group scales
     float* act;               // [T*k,I]    SiLU(gate)*up
     uint8_t* aq;              // [T*k,I]    requantised act
     float* as;                // [T*k,I/128]
@@ -77,6 +76,7 @@ struct KParams {
     // runtime shape and LDS layout
     int32_t T, E, k, renorm;
     int32_t naq;              // requantised-act LDS buffers (2 = double buffered, 1)
+    int32_t nslots;           // partial-sum hand-off slots (power of two)
 };
 
 // One compiled (H, I) specialisation.
@@ -103,9 +103,9 @@ __host__ __device__ inline int lds_region_bytes(int H, int I, int T, int naq) {
     const int m = up > dn ? up : dn;
     return (m + 15) & ~15;
 }
-__host__ __device__ inline int lds_partials_bytes() { return kSlots * kComputeWaves * 64 * 16; }
-__host__ __device__ inline int lds_dynamic_bytes(int H, int I, int T, int naq) {
-    return lds_region_bytes(H, I, T, naq) + lds_partials_bytes();
+__host__ __device__ inline int lds_partials_bytes(int nslots) { return nslots * kComputeWaves * 64 * 16; }
+__host__ __device__ inline int lds_dynamic_bytes(int H, int I, int T, int naq, int nslots) {
+    return lds_region_bytes(H, I, T, naq) + lds_partials_bytes(nslots);
 }
 
 }  // namespace monomoe
