@@ -103,9 +103,10 @@ int monomoe_forward(monomoe_plan_t plan, const void* x, const void* router_w,
  *                                 boundaries, for latency breakdowns (written)
  *   spin_limit_ticks              bound of every readiness wait in 100 MHz ticks
  *                                 (0 = the default of 2 s)
- *   fail_flag                     nonzero makes the routing wait target unreachable, so
- *                                 the kernel takes its timeout path and reports
- *                                 MONOMOE_ERR_TIMEOUT through monomoe_plan_status(). */
+ *   fail_flag                     nonzero makes every workgroup wait on a condition that
+ *                                 never holds (bounded by the spin limit), so the kernel
+ *                                 takes its timeout path and reports MONOMOE_ERR_TIMEOUT
+ *                                 through monomoe_plan_status(). */
 typedef struct {
     int32_t* topk_ids;
     float* topk_w;
@@ -132,8 +133,9 @@ int monomoe_forward_debug(monomoe_plan_t plan, const void* x, const void* router
  * status is sticky until monomoe_plan_reset(). */
 int monomoe_plan_status(monomoe_plan_t plan);
 
-/* Clear the status word and every readiness counter and accumulator of the plan's
- * workspace (needed only after a device-side error).  Blocking. */
+/* Zero the plan's workspace: status word, launch epochs, output-tile counters and the
+ * fp32 output accumulator (needed only after a device-side error, which can leave tile
+ * counters and the accumulator dirty).  Blocking. */
 int monomoe_plan_reset(monomoe_plan_t plan);
 
 /* Launch geometry and footprint of a plan, for tests and benchmarks. */

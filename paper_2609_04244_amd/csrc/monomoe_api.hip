@@ -26,10 +26,8 @@ struct monomoe_plan_s {
     void* ws;
     size_t ws_bytes;
     uint32_t* ctl;
-    float* logits;
-    float* act;
-    uint8_t* aq;
-    float* as;
+    uint64_t* logits;
+    uint64_t* act;
     float* out_acc;
 };
 
@@ -70,8 +68,6 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
     p.ctl = plan->ctl;
     p.logits = plan->logits;
     p.act = plan->act;
-    p.aq = plan->aq;
-    p.as = plan->as;
     p.out_acc = plan->out_acc;
     p.spin_limit = kDefaultSpinTicks;
     if (dbg) {
@@ -186,15 +182,17 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
         return MONOMOE_ERR_OCCUPANCY;
     }
     pl->grid = pl->num_cus;   // one resident workgroup per CU
+    if (pl->grid > kGridMax) {
+        delete pl;
+        return MONOMOE_ERR_UNSUPPORTED;
+    }
 
-    // workspace: control words | logits | act | aq | as | out_acc
+    // workspace: control words | logits | act | out_acc
     const int T = Tl;
     size_t off = 0;
-    const size_t o_ctl = off;    off = align_up(off + sizeof(uint32_t) * ctl_words(s.H, s.I), 256);
-    const size_t o_log = off;    off = align_up(off + sizeof(float) * (size_t)T * s.E, 256);
-    const size_t o_act = off;    off = align_up(off + sizeof(float) * (size_t)T * topk * s.I, 256);
-    const size_t o_aq = off;     off = align_up(off + (size_t)T * topk * s.I, 256);
-    const size_t o_as = off;     off = align_up(off + sizeof(float) * (size_t)T * topk * (s.I / 128), 256);
+    const size_t o_ctl = off;    off = align_up(off + sizeof(uint32_t) * ctl_words(s.H), 256);
+    const size_t o_log = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * s.E, 256);
+    const size_t o_act = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * topk * s.I, 256);
     const size_t o_out = off;    off = align_up(off + sizeof(float) * (size_t)T * s.H, 256);
     pl->ws_bytes = off;
     if (hipMalloc(&pl->ws, pl->ws_bytes) != hipSuccess) {
@@ -203,10 +201,8 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     }
     uint8_t* base = static_cast<uint8_t*>(pl->ws);
     pl->ctl = reinterpret_cast<uint32_t*>(base + o_ctl);
-    pl->logits = reinterpret_cast<float*>(base + o_log);
-    pl->act = reinterpret_cast<float*>(base + o_act);
-    pl->aq = base + o_aq;
-    pl->as = reinterpret_cast<float*>(base + o_as);
+    pl->logits = reinterpret_cast<uint64_t*>(base + o_log);
+    pl->act = reinterpret_cast<uint64_t*>(base + o_act);
     pl->out_acc = reinterpret_cast<float*>(base + o_out);
     const int zr = zero_workspace(pl);
     if (zr != MONOMOE_OK) {

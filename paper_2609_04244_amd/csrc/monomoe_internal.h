@@ -16,22 +16,24 @@ constexpr int kEMax = 512;                    // experts bound (8 logits per lan
 constexpr int kUMax = kTMax * kKMax;          // active experts bound (T*k, also <= E)
 constexpr int kSlotsMin = 4;                  // partial-sum hand-off slots per workgroup:
 constexpr int kSlotsMax = 32;                 //   a power of two in [min, max], as LDS allows
-constexpr int kXcds = 8;                      // XCDs; workgroups are dealt round-robin
 
-// Control words at the head of the workspace (uint32 each).  Every counter is zero
-// when no launch is in flight: the last user of each counter clears it, and the last
-// workgroup to leave a launch clears the rest.
+constexpr int kGridMax = 1024;                // persistent workgroups at most
+
+// Control words at the head of the workspace (uint32 each).
+//  * status: sticky device status (kDev*).
+//  * epoch[wg]: launches this workgroup has completed.  All workgroups advance in
+//    lockstep, so a launch's tag (epoch + 1) is the same everywhere; cross-workgroup
+//    data (logits, SiLU activations) is written as 8-byte words {value, tag}, and a
+//    reader knows a word is from this launch when its tag matches.  Nothing is reset
+//    between launches.
+//  * tile[H/16]: finished down units per 16-row output tile; the last contributor
+//    converts the tile and clears the counter (and the fp32 accumulator).
 enum : int {
-    kCtlRoute = 0,              // XCDs whose workgroups all published routing inputs
-    kCtlExit = 1,               // workgroups that finished the launch
-    kCtlStatus = 2,             // sticky device status (kDev*)
-    kCtlRouteXcd = 8,           // [kXcds] workgroups of each XCD that published
-    kCtlUp = 16,                // [kUMax] requantised 128-groups per active-expert slot
-    kCtlTile = kCtlUp + kUMax,  // [H/16] finished down units per 16-row output tile
+    kCtlStatus = 0,
+    kCtlEpoch = 64,                       // [kGridMax]
+    kCtlTile = kCtlEpoch + kGridMax,      // [H/16]
 };
-// then [kUMax * I/128] gate/up units finished per (active-expert slot, 128-group)
-constexpr int ctl_grp_offset(int H) { return kCtlTile + H / 16; }
-constexpr int ctl_words(int H, int I) { return ctl_grp_offset(H) + kUMax * (I / 128); }
+constexpr int ctl_words(int H) { return kCtlTile + H / 16; }
 
 enum : uint32_t { kDevOk = 0, kDevTimeout = 1, kDevBadIds = 2 };
 
@@ -54,10 +56,8 @@ struct KParams {
     uint16_t* out;            // bf16 [T,H]
     // plan workspace
     uint32_t* ctl;            // control words
-    float* logits;            // [T,E]
-    float* act;               // [T*k,I]    SiLU(gate)*up
-    uint8_t* aq;              // [T*k,I]    requantised act
-    float* as;                // [T*k,I/128]
+    uint64_t* logits;         // [T,E]   {fp32 logit, tag}
+    uint64_t* act;            // [T*k,I] {fp32 SiLU(gate)*up, tag}
     float* out_acc;           // [T,H]      fp32 accumulator, zero between launches
     // test hooks (null when unused)
     int32_t* d_ids;
