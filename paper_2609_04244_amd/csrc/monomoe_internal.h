@@ -92,10 +92,12 @@ const KernelEntry* kernel_at(int i);
 
 // Dynamic LDS: the phase-aliased region (quantised input during gate/up; `naq`
 // requantised-act buffers during down) followed by the partial-sum hand-off slots.
-// Rows are padded by 16 bytes; every buffer starts 16-byte aligned.
-__host__ __device__ inline int lds_up_bytes(int H, int T) { return T * (H + 16) + T * (H / 128) * 4; }
+// Code rows are padded by 16 bytes; the scale arrays always have kTMax rows (rows of
+// absent or unrouted tokens hold 0, which zeroes their MFMA columns); every buffer
+// starts 16-byte aligned.
+__host__ __device__ inline int lds_up_bytes(int H, int T) { return T * (H + 16) + kTMax * (H / 128) * 4; }
 __host__ __device__ inline int lds_aq_buffer_bytes(int I, int T) {
-    return (T * (I + 16) + T * (I / 128) * 4 + 15) & ~15;
+    return (T * (I + 16) + kTMax * (I / 128) * 4 + 15) & ~15;
 }
 __host__ __device__ inline int lds_region_bytes(int H, int I, int T, int naq) {
     const int up = lds_up_bytes(H, T);
@@ -103,6 +105,7 @@ __host__ __device__ inline int lds_region_bytes(int H, int I, int T, int naq) {
     const int m = up > dn ? up : dn;
     return (m + 15) & ~15;
 }
+// per slot, one 16x16 fp32 partial tile per compute wavefront
 __host__ __device__ inline int lds_partials_bytes(int nslots) { return nslots * kComputeWaves * 64 * 16; }
 __host__ __device__ inline int lds_dynamic_bytes(int H, int I, int T, int naq, int nslots) {
     return lds_region_bytes(H, I, T, naq) + lds_partials_bytes(nslots);
