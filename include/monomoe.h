@@ -133,9 +133,9 @@ int monomoe_forward_debug(monomoe_plan_t plan, const void* x, const void* router
  * status is sticky until monomoe_plan_reset(). */
 int monomoe_plan_status(monomoe_plan_t plan);
 
-/* Zero the plan's workspace: status word, launch epochs, output-tile counters and the
- * fp32 output accumulator (needed only after a device-side error, which can leave tile
- * counters and the accumulator dirty).  Blocking. */
+/* Zero the plan's workspace: the sticky status word, the launch epochs and the tagged
+ * exchange buffers (needed after a device-side error, which can leave workgroups out of
+ * step).  Blocking. */
 int monomoe_plan_reset(monomoe_plan_t plan);
 
 /* Launch geometry and footprint of a plan, for tests and benchmarks. */

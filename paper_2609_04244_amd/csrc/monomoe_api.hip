@@ -28,7 +28,7 @@ struct monomoe_plan_s {
     uint32_t* ctl;
     uint64_t* logits;
     uint64_t* act;
-    float* out_acc;
+    uint64_t* contrib;
 };
 
 namespace {
@@ -68,7 +68,7 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
     p.ctl = plan->ctl;
     p.logits = plan->logits;
     p.act = plan->act;
-    p.out_acc = plan->out_acc;
+    p.contrib = plan->contrib;
     p.spin_limit = kDefaultSpinTicks;
     if (dbg) {
         if ((dbg->topk_ids == nullptr) != (dbg->topk_w == nullptr)) return MONOMOE_ERR_INVALID;
@@ -187,13 +187,13 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
         return MONOMOE_ERR_UNSUPPORTED;
     }
 
-    // workspace: control words | logits | act | out_acc
+    // workspace: control words | logits | act | contrib
     const int T = Tl;
     size_t off = 0;
-    const size_t o_ctl = off;    off = align_up(off + sizeof(uint32_t) * ctl_words(s.H), 256);
+    const size_t o_ctl = off;    off = align_up(off + sizeof(uint32_t) * ctl_words(), 256);
     const size_t o_log = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * s.E, 256);
     const size_t o_act = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * topk * s.I, 256);
-    const size_t o_out = off;    off = align_up(off + sizeof(float) * (size_t)T * s.H, 256);
+    const size_t o_out = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * topk * s.H, 256);
     pl->ws_bytes = off;
     if (hipMalloc(&pl->ws, pl->ws_bytes) != hipSuccess) {
         delete pl;
@@ -203,7 +203,7 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     pl->ctl = reinterpret_cast<uint32_t*>(base + o_ctl);
     pl->logits = reinterpret_cast<uint64_t*>(base + o_log);
     pl->act = reinterpret_cast<uint64_t*>(base + o_act);
-    pl->out_acc = reinterpret_cast<float*>(base + o_out);
+    pl->contrib = reinterpret_cast<uint64_t*>(base + o_out);
     const int zr = zero_workspace(pl);
     if (zr != MONOMOE_OK) {
         (void)hipFree(pl->ws);

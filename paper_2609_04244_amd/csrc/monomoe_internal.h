@@ -23,25 +23,22 @@ constexpr int kGridMax = 1024;                // persistent workgroups at most
 //  * status: sticky device status (kDev*).
 //  * epoch[wg]: launches this workgroup has completed.  All workgroups advance in
 //    lockstep, so a launch's tag (epoch + 1) is the same everywhere; cross-workgroup
-//    data (logits, SiLU activations) is written as 8-byte words {value, tag}, and a
-//    reader knows a word is from this launch when its tag matches.  Nothing is reset
-//    between launches.
-//  * tile[H/16]: finished down units per 16-row output tile; the last contributor
-//    converts the tile and clears the counter (and the fp32 accumulator).
+//    data (logits, SiLU activations, output contributions) is written as 8-byte words
+//    {value, tag}, and a reader knows a word is from this launch when its tag matches.
+//    Nothing is reset between launches.
 enum : int {
     kCtlStatus = 0,
     kCtlEpoch = 64,                       // [kGridMax]
-    kCtlTile = kCtlEpoch + kGridMax,      // [H/16]
 };
-constexpr int ctl_words(int H) { return kCtlTile + H / 16; }
+constexpr int ctl_words() { return kCtlEpoch + kGridMax; }
 
 enum : uint32_t { kDevOk = 0, kDevTimeout = 1, kDevBadIds = 2 };
 
 // Phase stamps (test hook): per workgroup, s_memrealtime at these points.
 constexpr int kStamps = 16;
 enum : int {
-    kStEntry = 0, kStPublished, kStRouted, kStMeta, kStXqStaged, kStUpDone, kStFirstAq, kStDownDone,
-    kStExit, kStFirstMfma, kStComputeDone, kStRouter, kStQuant, kStTopk,
+    kStEntry = 0, kStPublished, kStRouted, kStMeta, kStUpComputed, kStUpDone, kStFirstAq, kStDownDone,
+    kStExit, kStFirstMfma, kStComputeDone, kStRouter, kStQuant, kStTopk, kStReduced,
 };
 
 struct KParams {
@@ -58,7 +55,7 @@ struct KParams {
     uint32_t* ctl;            // control words
     uint64_t* logits;         // [T,E]   {fp32 logit, tag}
     uint64_t* act;            // [T*k,I] {fp32 SiLU(gate)*up, tag}
-    float* out_acc;           // [T,H]      fp32 accumulator, zero between launches
+    uint64_t* contrib;        // [T*k,H] {fp32 routing-weighted expert output, tag}
     // test hooks (null when unused)
     int32_t* d_ids;
     float* d_w;

@@ -4,15 +4,23 @@ Hardware-counter runs profile a process that loads only the system HIP runtime a
 operator library (the C++ driver built from csrc/monomoe_profile.cpp), so the layers
 are generated here beforehand and saved as raw little-endian binaries:
 
-  generate: draw `--layers` synthetic layers of a workload on the GPU and save
-            DIR/l<l>_<field>.bin plus DIR/meta.txt ("H E I k renorm layers tmax has_bias");
-  run:      the same launches from Python through the ctypes binding (no profiler needed).
+  generate:  draw `--layers` synthetic layers of a workload on the GPU and save
+             DIR/l<l>_<field>.bin plus DIR/meta.txt ("H E I k renorm layers tmax has_bias");
+  run:       the same launches from Python through the ctypes binding (no profiler needed);
+  summarize: turn the CSV output of one --kernel-trace run and two --pmc runs (FETCH_SIZE,
+             WRITE_SIZE) of the C++ driver into a markdown summary and a JSON record: mean
+             launch duration per token count, HBM bytes per launch from the counters scaled by
+             what they read for the driver's plain copy kernel of known size, and the hash of
+             the kernel sources the counters belong to.
 
 Example:
   python3 -m paper_2609_04244_amd.profile_layer generate --workload small_expert --dir /tmp/moe
   rocprofv3 --kernel-trace --stats -d out -- paper_2609_04244_amd/monomoe_profile /tmp/moe 1,8 16 1024
 """
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -101,6 +109,124 @@ def run(args):
         print("reference copy and read kernels: %d MiB each, 3 launches" % args.copy_mib, flush=True)
 
 
+KERNEL_SOURCES = ("csrc/monomoe_kernel.hip", "csrc/monomoe_internal.h")
+
+
+def kernel_source_hash():
+    """sha256 over the fused kernel's sources (counters are only valid for this code)."""
+    h = hashlib.sha256()
+    here = os.path.dirname(os.path.abspath(__file__))
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(here, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def _rows(path):
+    files = glob.glob(os.path.join(path, "**", "*.csv"), recursive=True) if os.path.isdir(path) else [path]
+    return files
+
+
+def _find(path, suffix):
+    for f in _rows(path):
+        if f.endswith(suffix):
+            return f
+    raise FileNotFoundError("no *%s under %s" % (suffix, path))
+
+
+def _counter_by_dispatch(path, name):
+    """{dispatch_id: (kernel_name, value)} for counter `name` (summed over rows)."""
+    out = {}
+    with open(_find(path, "counter_collection.csv")) as fh:
+        for r in csv.DictReader(fh):
+            if r["Counter_Name"] != name:
+                continue
+            d = int(r["Dispatch_Id"])
+            k, v = out.get(d, (r["Kernel_Name"], 0.0))
+            out[d] = (k, v + float(r["Counter_Value"]))
+    return out
+
+
+def summarize(args):
+    Ts = [int(t) for t in args.T.split(",")]
+    n = args.iters
+    # kernel trace: durations of the fused launches in dispatch order
+    with open(_find(args.trace, "kernel_trace.csv")) as fh:
+        tr = [r for r in csv.DictReader(fh)]
+    tr.sort(key=lambda r: int(r["Dispatch_Id"]))
+    fused = [r for r in tr if "monomoe_fused" in r["Kernel_Name"]]
+    copies = [r for r in tr if "stream_copy" in r["Kernel_Name"]]
+    reads = [r for r in tr if "stream_read" in r["Kernel_Name"]]
+    if len(fused) != n * len(Ts):
+        raise SystemExit("expected %d fused launches in the trace, found %d" % (n * len(Ts), len(fused)))
+    dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3   # us
+    kname = fused[0]["Kernel_Name"]
+    per_T = {}
+    for i, T in enumerate(Ts):
+        d = [dur(r) for r in fused[i * n:(i + 1) * n]]
+        per_T[T] = {"launches": n, "us_mean": sum(d) / n, "us_min": min(d), "us_max": max(d)}
+    nbytes = args.copy_mib << 20
+    copy_us = min(dur(r) for r in copies) if copies else None
+    read_us = min(dur(r) for r in reads) if reads else None
+    rec = {
+        "kernel": kname, "workload": args.workload, "token_counts": Ts, "launches_per_T": n,
+        "kernel_source_sha256": kernel_source_hash(), "per_T": {},
+        "copy_kernel": {"bytes_each_way": nbytes, "us_min": copy_us,
+                        "GBps_read_plus_write": (2 * nbytes / copy_us / 1e3) if copy_us else None},
+        "read_kernel": {"bytes": nbytes, "us_min": read_us,
+                        "GBps": (nbytes / read_us / 1e3) if read_us else None},
+    }
+    if args.fetch and args.write:
+        fetch = _counter_by_dispatch(args.fetch, "FETCH_SIZE")
+        write = _counter_by_dispatch(args.write, "WRITE_SIZE")
+        for name, tab in (("fetch", fetch), ("write", write)):
+            ids = sorted(tab)
+            f_ids = [d for d in ids if "monomoe_fused" in tab[d][0]]
+            c_ids = [d for d in ids if "stream_copy" in tab[d][0]]
+            if len(f_ids) != n * len(Ts) or not c_ids:
+                raise SystemExit("%s pass: expected %d fused dispatches and the copy kernel" % (name, n * len(Ts)))
+            copy_kib = sum(tab[d][1] for d in c_ids) / len(c_ids)
+            factor = nbytes / (copy_kib * 1024.0)   # true bytes per counted byte
+            rec[name + "_calibration"] = {"copy_counter_KiB": copy_kib, "expected_KiB": nbytes / 1024.0,
+                                          "factor": factor}
+            for i, T in enumerate(Ts):
+                v = [tab[d][1] for d in f_ids[i * n:(i + 1) * n]]
+                kib = sum(v) / n
+                rec["per_T"].setdefault(str(T), {})[name + "_KiB_raw"] = kib
+                rec["per_T"][str(T)][name + "_bytes"] = kib * 1024.0 * factor
+    for T in Ts:
+        rec["per_T"].setdefault(str(T), {}).update(per_T[T])
+    os.makedirs(os.path.dirname(os.path.abspath(args.out_json)), exist_ok=True)
+    with open(args.out_json, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    lines = ["# %s on the %s workload" % (kname.split("(")[0], args.workload), "",
+             "Command (from the repository root; DIR and OUT are scratch directories):", "", "```",
+             args.command.strip(), "```", "",
+             "Kernel source sha256: `%s`" % rec["kernel_source_sha256"], "",
+             "| T | launches | mean us | min us | max us | HBM read (calibrated) | HBM write (calibrated) |",
+             "|---|---|---|---|---|---|---|"]
+    for T in Ts:
+        q = rec["per_T"][str(T)]
+        rd = "%.1f MB" % (q["fetch_bytes"] / 1e6) if "fetch_bytes" in q else "-"
+        wr = "%.2f MB" % (q["write_bytes"] / 1e6) if "write_bytes" in q else "-"
+        lines.append("| %d | %d | %.2f | %.2f | %.2f | %s | %s |" % (T, n, q["us_mean"], q["us_min"], q["us_max"], rd, wr))
+    lines.append("")
+    if copy_us:
+        lines.append("Plain copy kernel, %d MiB each way: %.1f us (%.0f GB/s read+write)." %
+                     (args.copy_mib, copy_us, rec["copy_kernel"]["GBps_read_plus_write"]))
+    if read_us:
+        lines.append("Plain read kernel, %d MiB: %.1f us (%.0f GB/s)." % (args.copy_mib, read_us, rec["read_kernel"]["GBps"]))
+    for name in ("fetch", "write"):
+        c = rec.get(name + "_calibration")
+        if c:
+            lines.append("%s counter on the copy kernel: %.0f KiB for %.0f KiB moved (factor %.4f)." %
+                         ("FETCH_SIZE" if name == "fetch" else "WRITE_SIZE", c["copy_counter_KiB"], c["expected_KiB"],
+                          c["factor"]))
+    with open(args.out_md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -115,11 +241,24 @@ def main():
     r.add_argument("--T", default="1,8")
     r.add_argument("--iters", type=int, default=16)
     r.add_argument("--copy-mib", type=int, default=0)
+    m = sub.add_parser("summarize")
+    m.add_argument("--trace", required=True, help="output directory of the --kernel-trace run")
+    m.add_argument("--fetch", help="output directory of the --pmc FETCH_SIZE run")
+    m.add_argument("--write", help="output directory of the --pmc WRITE_SIZE run")
+    m.add_argument("--T", default="1,2,4,8")
+    m.add_argument("--iters", type=int, required=True)
+    m.add_argument("--copy-mib", type=int, default=1024)
+    m.add_argument("--workload", default="small_expert")
+    m.add_argument("--command", default="", help="the command lines that produced the runs")
+    m.add_argument("--out-md", required=True)
+    m.add_argument("--out-json", required=True)
     args = ap.parse_args()
     if args.cmd == "generate":
         generate(args)
-    else:
+    elif args.cmd == "run":
         run(args)
+    else:
+        summarize(args)
 
 
 if __name__ == "__main__":
