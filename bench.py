@@ -27,6 +27,11 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
 TS = (1, 2, 4, 8)
+# HBM counter record of this workload (rocprofv3 FETCH_SIZE / WRITE_SIZE passes over the
+# C++ profiling driver, calibrated on a plain copy kernel); used only while the kernel
+# sources still hash to the value it was taken on.
+COUNTERS = os.path.join(ROOT, "profiles", "monomoe_fused_small_expert_counters.json")
+HOLD_CYCLES_PER_LAUNCH = 200_000   # GPU clock cycles of stream hold per timed launch (~80 us)
 
 
 def parse():
@@ -48,6 +53,24 @@ def algorithmic_bytes(U, T, H, E, I):
     weights = U * 3 * H * I
     scales = U * 3 * (H // 128) * (I // 128) * 4
     return weights + scales + E * H * 2 + 2 * T * H * 2
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch (read + write, mean over the step's token counts) from the
+    committed counter record, or None when there is none for this workload or the kernel
+    sources changed since it was taken."""
+    try:
+        with open(COUNTERS) as fh:
+            rec = json.load(fh)
+    except OSError:
+        return None
+    from paper_2609_04244_amd.profile_layer import kernel_source_hash
+    if rec.get("workload") != workload or rec.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    per = rec["per_T"]
+    if any(str(T) not in per or "fetch_bytes" not in per[str(T)] for T in TS):
+        return None
+    return sum(per[str(T)]["fetch_bytes"] + per[str(T)]["write_bytes"] for T in TS) / len(TS)
 
 
 def main():
@@ -113,6 +136,9 @@ def main():
     for i, (s, T) in enumerate(order):
         if s == args.warmup and t_start is None:
             torch.cuda.synchronize()
+            # hold the stream while the host enqueues the whole timed region, so that launches
+            # run back to back and the event pairs time the kernels, not host submission
+            torch.cuda._sleep(int(HOLD_CYCLES_PER_LAUNCH * args.steps * len(TS)) + 20_000_000)
             t_start = time.perf_counter()
             w_start.record(stream)
         ev0[i].record(stream)
@@ -156,6 +182,7 @@ def main():
         wbytes_tot += float(np.sum(wb))
     value = tot_bytes / (tot_ms * 1e-3) / 1e9
     ms_per_step = w_start.elapsed_time(w_end) / args.steps
+    traffic = measured_traffic(args.workload)
 
     res = {
         "metric": "routed-MoE op latency us + achieved HBM GB/s (% of peak) at T=1,2,4,8 tokens",
@@ -171,7 +198,10 @@ def main():
         "per_T": per_T,
         "roofline": {
             "bound": "hbm", "achieved": round(float(value), 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-            "frac": round(float(value / PEAK_HBM_GBPS), 4), "traffic": None,
+            "frac": round(float(value / PEAK_HBM_GBPS), 4),
+            "traffic": None if traffic is None else round(float(traffic)),
+            "traffic_unit": "HBM bytes per launch (read + write, mean over T)",
+            "algorithmic_bytes_per_launch": round(float(tot_bytes / (args.steps * len(TS)))),
             "kernel": "monomoe_fused<%d,%d>" % (H, I),
             "launch_us_mean": round(float(tot_ms / (args.steps * len(TS)) * 1e3), 2),
         },

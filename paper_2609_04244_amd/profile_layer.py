@@ -7,6 +7,8 @@ are generated here beforehand and saved as raw little-endian binaries:
   generate:  draw `--layers` synthetic layers of a workload on the GPU and save
              DIR/l<l>_<field>.bin plus DIR/meta.txt ("H E I k renorm layers tmax has_bias");
   run:       the same launches from Python through the ctypes binding (no profiler needed);
+  bench:     summarise a --kernel-trace --stats run of bench.py itself: the fused kernel's
+             timed launches (the last --timed ones) against bench.py's own event timing;
   summarize: turn the CSV output of one --kernel-trace run and two --pmc runs (FETCH_SIZE,
              WRITE_SIZE) of the C++ driver into a markdown summary and a JSON record: mean
              launch duration per token count, HBM bytes per launch from the counters scaled by
@@ -194,8 +196,25 @@ def summarize(args):
                 kib = sum(v) / n
                 rec["per_T"].setdefault(str(T), {})[name + "_KiB_raw"] = kib
                 rec["per_T"][str(T)][name + "_bytes"] = kib * 1024.0 * factor
+    if args.mfma:
+        busy = _counter_by_dispatch(args.mfma, "SQ_VALU_MFMA_BUSY_CYCLES")
+        gui = _counter_by_dispatch(args.mfma, "GRBM_GUI_ACTIVE")
+        f_ids = [d for d in sorted(busy) if "monomoe_fused" in busy[d][0]]
+        if len(f_ids) == n * len(Ts):
+            for i, T in enumerate(Ts):
+                ids = f_ids[i * n:(i + 1) * n]
+                b = sum(busy[d][1] for d in ids) / n
+                g = sum(gui[d][1] for d in ids) / n
+                # GRBM_GUI_ACTIVE sums the XCDs' clocks; SQ_VALU_MFMA_BUSY_CYCLES sums the CUs
+                rec["per_T"].setdefault(str(T), {}).update(
+                    {"mfma_busy_cycles": b, "gui_active_cycles": g,
+                     "mfma_busy_frac": b / (g / args.xcds * args.cus) if g > 0 else None})
     for T in Ts:
         rec["per_T"].setdefault(str(T), {}).update(per_T[T])
+    stats = [f for f in _rows(args.trace) if f.endswith("kernel_stats.csv")]
+    if stats:
+        with open(stats[0]) as fh:
+            rec["kernel_stats"] = [r for r in csv.DictReader(fh)]
     os.makedirs(os.path.dirname(os.path.abspath(args.out_json)), exist_ok=True)
     with open(args.out_json, "w") as fh:
         json.dump(rec, fh, indent=1)
@@ -222,6 +241,49 @@ def summarize(args):
             lines.append("%s counter on the copy kernel: %.0f KiB for %.0f KiB moved (factor %.4f)." %
                          ("FETCH_SIZE" if name == "fetch" else "WRITE_SIZE", c["copy_counter_KiB"], c["expected_KiB"],
                           c["factor"]))
+    if any("mfma_busy_frac" in rec["per_T"][str(T)] for T in Ts):
+        lines.append("MFMA busy per CU (SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / %d XCDs x %d CUs)): %s." % (
+            args.xcds, args.cus, ", ".join("T=%d %.1f%%" % (T, 100 * rec["per_T"][str(T)]["mfma_busy_frac"]) for T in Ts
+                                if rec["per_T"][str(T)].get("mfma_busy_frac") is not None)))
+    if rec.get("kernel_stats"):
+        lines += ["", "rocprofv3 --stats (all launches of the run):", "",
+                  "| kernel | calls | average ns | min ns | max ns |", "|---|---|---|---|---|"]
+        for r in rec["kernel_stats"]:
+            lines.append("| %s | %s | %s | %s | %s |" % (r.get("Name", "")[:60], r.get("Calls", ""),
+                         r.get("AverageNs", ""), r.get("MinNs", ""), r.get("MaxNs", "")))
+    with open(args.out_md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def bench_trace(args):
+    with open(_find(args.trace, "kernel_trace.csv")) as fh:
+        tr = [r for r in csv.DictReader(fh) if "monomoe_fused" in r["Kernel_Name"]]
+    tr.sort(key=lambda r: int(r["Dispatch_Id"]))
+    timed = tr[-args.timed:]
+    d = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in timed]
+    with open(args.bench_json) as fh:
+        b = json.loads(fh.read().strip().splitlines()[-1])
+    stats = [f for f in _rows(args.trace) if f.endswith("kernel_stats.csv")]
+    lines = ["# bench.py under rocprofv3 --kernel-trace --stats", "",
+             "Command (from the repository root; OUT is a scratch directory):", "", "```", args.command.strip(), "```", "",
+             "Kernel source sha256: `%s`" % kernel_source_hash(), "",
+             "Fused-kernel launches in the trace: %d (selection pass, warm-up and timed); the last %d are the "
+             "timed ones." % (len(tr), len(timed)), "",
+             "| source | mean launch us |", "|---|---|",
+             "| rocprofv3 kernel trace, timed launches | %.2f |" % (sum(d) / len(d)),
+             "| bench.py HIP events (roofline.launch_us_mean) | %.2f |" % b["roofline"]["launch_us_mean"], ""]
+    lines.append("bench.py line: value %.1f GB/s (%.1f%% of 8 TB/s); per T: %s." % (
+        b["value"], 100 * b["roofline"]["frac"],
+        ", ".join("T=%s %.2f us" % (k, v["us_mean"]) for k, v in b["per_T"].items())))
+    if stats:
+        with open(stats[0]) as fh:
+            rows = [r for r in csv.DictReader(fh)]
+        lines += ["", "rocprofv3 --stats (every launch of the process):", "",
+                  "| kernel | calls | average ns | min ns | max ns |", "|---|---|---|---|---|"]
+        for r in rows[:8]:
+            lines.append("| %s | %s | %s | %s | %s |" % (r.get("Name", "")[:60], r.get("Calls", ""),
+                         r.get("AverageNs", ""), r.get("MinNs", ""), r.get("MaxNs", "")))
     with open(args.out_md, "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print("\n".join(lines))
@@ -245,6 +307,9 @@ def main():
     m.add_argument("--trace", required=True, help="output directory of the --kernel-trace run")
     m.add_argument("--fetch", help="output directory of the --pmc FETCH_SIZE run")
     m.add_argument("--write", help="output directory of the --pmc WRITE_SIZE run")
+    m.add_argument("--mfma", help="output directory of a --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE run")
+    m.add_argument("--cus", type=int, default=256)
+    m.add_argument("--xcds", type=int, default=8)
     m.add_argument("--T", default="1,2,4,8")
     m.add_argument("--iters", type=int, required=True)
     m.add_argument("--copy-mib", type=int, default=1024)
@@ -252,8 +317,16 @@ def main():
     m.add_argument("--command", default="", help="the command lines that produced the runs")
     m.add_argument("--out-md", required=True)
     m.add_argument("--out-json", required=True)
+    bt = sub.add_parser("bench")
+    bt.add_argument("--trace", required=True)
+    bt.add_argument("--timed", type=int, required=True, help="timed launches (steps x token counts)")
+    bt.add_argument("--bench-json", required=True, help="bench.py's output line")
+    bt.add_argument("--command", default="")
+    bt.add_argument("--out-md", required=True)
     args = ap.parse_args()
-    if args.cmd == "generate":
+    if args.cmd == "bench":
+        bench_trace(args)
+    elif args.cmd == "generate":
         generate(args)
     elif args.cmd == "run":
         run(args)
