@@ -5,8 +5,10 @@ One step = one forward of the operator for each decode token count T in {1, 2, 4
 the small-expert layer shape (H=2048, E=128, I=768, top-8, renormalised softmax), each
 forward on its own synthetic layer.  Layers rotate over `--layers` distinct weight sets
 so that successive launches stream weights from HBM rather than from the 256 MB
-last-level cache (as consecutive MoE layers of a decode step do).  Every launch is timed
-with a pair of HIP events on the stream it runs on.
+last-level cache (as consecutive MoE layers of a decode step do).
+
+Each launch's duration comes from HIP events that its own dispatch stamps (hipExtLaunchKernel
+through monomoe_forward_timed): the kernel's begin and end, as a kernel trace reports them.
 
 Printed (one JSON line): value = algorithmic bytes of the step / summed launch time (GB/s);
 per-T latency (mean and p50, microseconds), achieved GB/s and fraction of the 8 TB/s peak;
@@ -31,7 +33,6 @@ TS = (1, 2, 4, 8)
 # C++ profiling driver, calibrated on a plain copy kernel); used only while the kernel
 # sources still hash to the value it was taken on.
 COUNTERS = os.path.join(ROOT, "profiles", "monomoe_fused_small_expert_counters.json")
-HOLD_CYCLES_PER_LAUNCH = 200_000   # GPU clock cycles of stream hold per timed launch (~80 us)
 
 
 def parse():
@@ -95,13 +96,12 @@ def main():
     outs = {T: torch.empty((T, H), dtype=torch.bfloat16, device=dev) for T in TS}
     xs = {(l, T): layers[l]["x"][:T].contiguous() for l in range(args.layers) for T in TS}
 
-    def launch(l, T):
+    def launch(l, T, timer):
         L = layers[l]
         p = plans[T]
         if L["bias"] is not None:
             p.set_router_bias(L["bias"])
-        p.forward(xs[(l, T)], L["router_w"], L["w13"], L["w13_scale"], L["w2"], L["w2_scale"], out=outs[T],
-                  check=False)
+        p.forward_timed(xs[(l, T)], L["router_w"], L["w13"], L["w13_scale"], L["w2"], L["w2_scale"], outs[T], timer)
 
     # unique experts of every (layer, T), from the operator's own selection (untimed)
     U = {}
@@ -121,8 +121,8 @@ def main():
     stream = torch.cuda.current_stream()
     order = [(s, T) for s in range(args.warmup + args.steps) for T in TS]
     n_launch = len(order)
-    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(n_launch)]
-    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(n_launch)]
+    # each launch's dispatch stamps its own begin and end (hipExtLaunchKernel events)
+    timers = [mm.DispatchTimer() for _ in range(n_launch)]
     layer_of = []
     li = 0
     for i in range(n_launch):
@@ -136,14 +136,9 @@ def main():
     for i, (s, T) in enumerate(order):
         if s == args.warmup and t_start is None:
             torch.cuda.synchronize()
-            # hold the stream while the host enqueues the whole timed region, so that launches
-            # run back to back and the event pairs time the kernels, not host submission
-            torch.cuda._sleep(int(HOLD_CYCLES_PER_LAUNCH * args.steps * len(TS)) + 20_000_000)
             t_start = time.perf_counter()
             w_start.record(stream)
-        ev0[i].record(stream)
-        launch(layer_of[i], T)
-        ev1[i].record(stream)
+        launch(layer_of[i], T, timers[i])
     w_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
@@ -161,7 +156,7 @@ def main():
         for i, (s, TT) in enumerate(order):
             if s < args.warmup or TT != T:
                 continue
-            ms.append(ev0[i].elapsed_time(ev1[i]))
+            ms.append(timers[i].elapsed_ms())
             u = U[(layer_of[i], T)]
             by.append(algorithmic_bytes(u, T, H, E, I))
             wb.append(u * 3 * H * I)

@@ -128,6 +128,16 @@ int monomoe_forward_debug(monomoe_plan_t plan, const void* x, const void* router
                           const void* w2, const float* w2_scale,
                           void* out, const monomoe_debug_t* dbg, hipStream_t stream);
 
+/* Measurement hook: monomoe_forward with the kernel launched through hipExtLaunchKernel,
+ * so that `start` and `stop` (caller-created hipEvents, both non-NULL) take the dispatch's
+ * own begin and end timestamps instead of the stream positions around it; the elapsed
+ * time between them is the kernel duration that a kernel trace reports.  Same arguments,
+ * errors and asynchrony as monomoe_forward. */
+int monomoe_forward_timed(monomoe_plan_t plan, const void* x, const void* router_w,
+                          const void* w13, const float* w13_scale,
+                          const void* w2, const float* w2_scale,
+                          void* out, hipEvent_t start, hipEvent_t stop, hipStream_t stream);
+
 /* Device-side status of the plan's last launches: MONOMOE_OK or MONOMOE_ERR_TIMEOUT.
  * Blocking: copies the status word to the host after a device synchronisation.  The
  * status is sticky until monomoe_plan_reset(). */

@@ -3,6 +3,8 @@
 #include "../../include/monomoe.h"
 #include "monomoe_internal.h"
 
+#include <hip/hip_ext.h>
+
 #include <new>
 #include <string.h>
 
@@ -46,7 +48,8 @@ int zero_workspace(monomoe_plan_s* pl) {
 }
 
 int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void* w13, const float* w13_scale,
-           const void* w2, const float* w2_scale, void* out, const monomoe_debug_t* dbg, hipStream_t stream) {
+           const void* w2, const float* w2_scale, void* out, const monomoe_debug_t* dbg, hipStream_t stream,
+           hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr) {
     if (!plan) return MONOMOE_ERR_INVALID;
     const monomoe_shape_t& s = plan->shape;
     if (s.T == 0) return MONOMOE_OK;
@@ -98,7 +101,15 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
 
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess || cur != plan->device) return MONOMOE_ERR_INVALID;
-    plan->kern->launch(p, plan->grid, (size_t)plan->lds_dyn, stream);
+    if (ev_start || ev_stop) {
+        // the dispatch itself records the events (its begin and end), not the stream
+        void* args[] = {&p};
+        if (hipExtLaunchKernel(plan->kern->fn, dim3(plan->grid), dim3(kThreads), args, (size_t)plan->lds_dyn, stream,
+                               ev_start, ev_stop, 0) != hipSuccess)
+            return MONOMOE_ERR_HIP;
+    } else {
+        plan->kern->launch(p, plan->grid, (size_t)plan->lds_dyn, stream);
+    }
     if (hipGetLastError() != hipSuccess) return MONOMOE_ERR_HIP;
     return MONOMOE_OK;
 }
@@ -230,6 +241,13 @@ int monomoe_plan_set_router_bias(monomoe_plan_t plan, const float* bias) {
 int monomoe_forward(monomoe_plan_t plan, const void* x, const void* router_w, const void* w13,
                     const float* w13_scale, const void* w2, const float* w2_scale, void* out, hipStream_t stream) {
     return launch(plan, x, router_w, w13, w13_scale, w2, w2_scale, out, nullptr, stream);
+}
+
+int monomoe_forward_timed(monomoe_plan_t plan, const void* x, const void* router_w, const void* w13,
+                          const float* w13_scale, const void* w2, const float* w2_scale, void* out,
+                          hipEvent_t start, hipEvent_t stop, hipStream_t stream) {
+    if (!start || !stop) return MONOMOE_ERR_INVALID;
+    return launch(plan, x, router_w, w13, w13_scale, w2, w2_scale, out, nullptr, stream, start, stop);
 }
 
 int monomoe_forward_debug(monomoe_plan_t plan, const void* x, const void* router_w, const void* w13,

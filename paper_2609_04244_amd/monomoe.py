@@ -22,7 +22,7 @@ MONOMOE_ERR_TIMEOUT = -5
 # Every symbol include/monomoe.h declares.
 EXPORTS = (
     "monomoe_plan", "monomoe_plan_destroy", "monomoe_plan_set_router_bias", "monomoe_forward",
-    "monomoe_forward_debug", "monomoe_plan_status", "monomoe_plan_reset", "monomoe_plan_info",
+    "monomoe_forward_debug", "monomoe_forward_timed", "monomoe_plan_status", "monomoe_plan_reset", "monomoe_plan_info",
     "monomoe_supported_shape", "monomoe_status_string", "monomoe_stream_copy", "monomoe_stream_read",
 )
 
@@ -72,6 +72,8 @@ def lib():
         L.monomoe_forward.restype = ctypes.c_int
         L.monomoe_forward_debug.argtypes = [vp] * 8 + [ctypes.POINTER(Debug), vp]
         L.monomoe_forward_debug.restype = ctypes.c_int
+        L.monomoe_forward_timed.argtypes = [vp] * 11
+        L.monomoe_forward_timed.restype = ctypes.c_int
         L.monomoe_plan_status.argtypes = [vp]
         L.monomoe_plan_status.restype = ctypes.c_int
         L.monomoe_plan_reset.argtypes = [vp]
@@ -112,6 +114,59 @@ def stream_read(src, sink, nbytes=None, stream=None):
     rc = lib().monomoe_stream_read(ctypes.c_void_p(src.data_ptr()), n, ctypes.c_void_p(sink.data_ptr()), _stream(stream))
     if rc != MONOMOE_OK:
         raise MonoMoEError(rc, "monomoe_stream_read")
+
+
+_hip = None
+
+
+def _hip_runtime():
+    """The HIP runtime already loaded by torch (events for monomoe_forward_timed)."""
+    global _hip
+    if _hip is None:
+        import torch  # noqa: F401  (loads the runtime first)
+        h = None
+        for name in ("libamdhip64.so.7", "libamdhip64.so"):
+            try:
+                h = ctypes.CDLL(name)
+                break
+            except OSError:
+                continue
+        if h is None:
+            raise RuntimeError("HIP runtime library not found")
+        vp = ctypes.c_void_p
+        h.hipEventCreate.argtypes = [ctypes.POINTER(vp)]
+        h.hipEventCreate.restype = ctypes.c_int
+        h.hipEventDestroy.argtypes = [vp]
+        h.hipEventDestroy.restype = ctypes.c_int
+        h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), vp, vp]
+        h.hipEventElapsedTime.restype = ctypes.c_int
+        _hip = h
+    return _hip
+
+
+class DispatchTimer:
+    """A pair of HIP events that monomoe_forward_timed stamps with the kernel dispatch's own
+    begin and end."""
+
+    def __init__(self):
+        h = _hip_runtime()
+        self.start, self.stop = ctypes.c_void_p(), ctypes.c_void_p()
+        if h.hipEventCreate(ctypes.byref(self.start)) or h.hipEventCreate(ctypes.byref(self.stop)):
+            raise RuntimeError("hipEventCreate failed")
+
+    def elapsed_ms(self):
+        ms = ctypes.c_float()
+        if _hip_runtime().hipEventElapsedTime(ctypes.byref(ms), self.start, self.stop):
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(ms.value)
+
+    def __del__(self):
+        try:
+            h = _hip_runtime()
+            h.hipEventDestroy(self.start)
+            h.hipEventDestroy(self.stop)
+        except Exception:
+            pass
 
 
 def _ptr(t):
@@ -188,6 +243,14 @@ class Plan:
                                    _ptr(w2_scale), _ptr(out), _stream(stream))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_forward")
+        return out
+
+    def forward_timed(self, x, router_w, w13, w13_scale, w2, w2_scale, out, timer, stream=None):
+        """monomoe_forward whose dispatch stamps `timer` (a DispatchTimer) with its own begin/end."""
+        rc = lib().monomoe_forward_timed(self._h, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale), _ptr(w2),
+                                         _ptr(w2_scale), _ptr(out), timer.start, timer.stop, _stream(stream))
+        if rc != MONOMOE_OK:
+            raise MonoMoEError(rc, "monomoe_forward_timed")
         return out
 
     def forward_debug(self, x, router_w, w13, w13_scale, w2, w2_scale, out=None, ids_in=None, w_in=None,

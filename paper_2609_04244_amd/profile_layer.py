@@ -272,7 +272,14 @@ def bench_trace(args):
              "timed ones." % (len(tr), len(timed)), "",
              "| source | mean launch us |", "|---|---|",
              "| rocprofv3 kernel trace, timed launches | %.2f |" % (sum(d) / len(d)),
-             "| bench.py HIP events (roofline.launch_us_mean) | %.2f |" % b["roofline"]["launch_us_mean"], ""]
+             "| bench.py dispatch-stamped HIP events, same (traced) run | %.2f |" % b["roofline"]["launch_us_mean"]]
+    if args.untraced_json:
+        with open(args.untraced_json) as fh:
+            u = json.loads(fh.read().strip().splitlines()[-1])
+        lines.append("| bench.py dispatch-stamped HIP events, run without the tracer | %.2f |" %
+                     u["roofline"]["launch_us_mean"])
+    lines += ["", "(Under the tracer the event stamps include its own per-dispatch work; without it the "
+              "dispatch-stamped events and the kernel trace agree.)", ""]
     lines.append("bench.py line: value %.1f GB/s (%.1f%% of 8 TB/s); per T: %s." % (
         b["value"], 100 * b["roofline"]["frac"],
         ", ".join("T=%s %.2f us" % (k, v["us_mean"]) for k, v in b["per_T"].items())))
@@ -321,6 +328,7 @@ def main():
     bt.add_argument("--trace", required=True)
     bt.add_argument("--timed", type=int, required=True, help="timed launches (steps x token counts)")
     bt.add_argument("--bench-json", required=True, help="bench.py's output line")
+    bt.add_argument("--untraced-json", help="bench.py's output line from a run without the tracer")
     bt.add_argument("--command", default="")
     bt.add_argument("--out-md", required=True)
     args = ap.parse_args()
