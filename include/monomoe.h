@@ -99,7 +99,7 @@ int monomoe_forward(monomoe_plan_t plan, const void* x, const void* router_w,
  *   out_f32   fp32  [T,H]         the weighted sum before rounding to bf16 (written)
  *   topk_ids_in / topk_w_in       [T,topk] replace the kernel's own selection (read);
  *                                 both or neither; ids distinct per token, in [0,E)
- *   stamps    u64   [grid,16]     per-workgroup s_memrealtime (100 MHz) stamps at phase
+ *   stamps    u64   [grid,24]     per-workgroup s_memrealtime (100 MHz) stamps at phase
  *                                 boundaries, for latency breakdowns (written)
  *   spin_limit_ticks              bound of every readiness wait in 100 MHz ticks
  *                                 (0 = the default of 2 s)

@@ -35,10 +35,10 @@ constexpr int ctl_words() { return kCtlEpoch + kGridMax; }
 enum : uint32_t { kDevOk = 0, kDevTimeout = 1, kDevBadIds = 2 };
 
 // Phase stamps (test hook): per workgroup, s_memrealtime at these points.
-constexpr int kStamps = 16;
+constexpr int kStamps = 24;
 enum : int {
-    kStEntry = 0, kStPublished, kStRouted, kStMeta, kStUpComputed, kStUpDone, kStFirstAq, kStDownDone,
-    kStExit, kStFirstMfma, kStComputeDone, kStRouter, kStQuant, kStTopk, kStReduced,
+    kStEntry = 0, kStIssued, kStFirstData, kStMeta, kStUpComputed, kStUpDone, kStFirstAq, kStDownDone,
+    kStExit, kStFirstMfma, kStComputeDone, kStRouter, kStQuant, kStTopk, kStReduced, kStLogits, kStSelected,
 };
 
 struct KParams {

@@ -270,7 +270,7 @@ class Plan:
             "aq": torch.zeros((T * k, I), dtype=torch.uint8, device=dev),
             "as": torch.zeros((T * k, I // 128), dtype=torch.float32, device=dev),
             "out_f32": torch.zeros((T, H), dtype=torch.float32, device=dev),
-            "stamps": torch.zeros((self.info()["grid"], 16), dtype=torch.int64, device=dev),
+            "stamps": torch.zeros((self.info()["grid"], 24), dtype=torch.int64, device=dev),
         }
         if (ids_in is None) != (w_in is None):
             raise ValueError("ids_in and w_in go together")
