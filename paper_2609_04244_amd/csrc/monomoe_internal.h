@@ -38,7 +38,7 @@ enum : uint32_t { kDevOk = 0, kDevTimeout = 1, kDevBadIds = 2 };
 constexpr int kStamps = 24;
 enum : int {
     kStEntry = 0, kStIssued, kStFirstData, kStMeta, kStUpComputed, kStUpDone, kStFirstAq, kStDownDone,
-    kStExit, kStFirstMfma, kStComputeDone, kStRouter, kStQuant, kStTopk, kStReduced, kStLogits, kStSelected,
+    kStExit, kStFirstMfma, kStComputeDone, kStRouter, kStQuant, kStTopk, kStReduced, kStLogits, kStSelected, kStSeek, kStLbase,
 };
 
 struct KParams {
