@@ -222,13 +222,19 @@ def summarize(args):
              "Command (from the repository root; DIR and OUT are scratch directories):", "", "```",
              args.command.strip(), "```", "",
              "Kernel source sha256: `%s`" % rec["kernel_source_sha256"], "",
-             "| T | launches | mean us | min us | max us | HBM read (calibrated) | HBM write (calibrated) |",
-             "|---|---|---|---|---|---|---|"]
+             "| T | launches | mean us | min us | max us | HBM read (calibrated) | HBM write (calibrated) "
+             "| HBM GB/s (read+write / mean) | % of 8 TB/s |",
+             "|---|---|---|---|---|---|---|---|---|"]
     for T in Ts:
         q = rec["per_T"][str(T)]
         rd = "%.1f MB" % (q["fetch_bytes"] / 1e6) if "fetch_bytes" in q else "-"
         wr = "%.2f MB" % (q["write_bytes"] / 1e6) if "write_bytes" in q else "-"
-        lines.append("| %d | %d | %.2f | %.2f | %.2f | %s | %s |" % (T, n, q["us_mean"], q["us_min"], q["us_max"], rd, wr))
+        bw, frac = "-", "-"
+        if "fetch_bytes" in q and "write_bytes" in q:
+            g = (q["fetch_bytes"] + q["write_bytes"]) / (q["us_mean"] * 1e-6) / 1e9
+            bw, frac = "%.0f" % g, "%.1f" % (100.0 * g / 8000.0)
+        lines.append("| %d | %d | %.2f | %.2f | %.2f | %s | %s | %s | %s |" %
+                     (T, n, q["us_mean"], q["us_min"], q["us_max"], rd, wr, bw, frac))
     lines.append("")
     if copy_us:
         lines.append("Plain copy kernel, %d MiB each way: %.1f us (%.0f GB/s read+write)." %
