@@ -156,6 +156,8 @@ typedef struct {
     int32_t occupancy;       /* workgroups per CU the occupancy API allows  */
     int32_t num_cus;
     int64_t workspace_bytes;
+    int32_t scratch_bytes;   /* per-thread private (scratch) memory of the kernel: 0 when
+                                all of its state lives in registers and LDS            */
 } monomoe_plan_info_t;
 
 int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info);

@@ -21,6 +21,7 @@ struct monomoe_plan_s {
     int grid;
     int lds_dyn;
     int lds_static;
+    int scratch;
     int naq;
     int nslots;
     const float* bias;
@@ -164,6 +165,7 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
         return MONOMOE_ERR_HIP;
     }
     pl->lds_static = (int)attr.sharedSizeBytes;
+    pl->scratch = (int)attr.localSizeBytes;
     // double-buffer the requantised activation in LDS when it fits, else single-buffer;
     // then as many partial-sum slots as the rest of the LDS holds (more slots let the
     // compute wavefronts run further ahead of the helper's epilogues)
@@ -280,6 +282,7 @@ int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info) {
     info->occupancy = plan->occupancy;
     info->num_cus = plan->num_cus;
     info->workspace_bytes = (int64_t)plan->ws_bytes;
+    info->scratch_bytes = plan->scratch;
     return MONOMOE_OK;
 }
 
