@@ -158,6 +158,43 @@ void mo_select(int T, int E, int k, int renorm, const double* logits, int32_t* i
 }
 
 /* ---------------------------------------------------------------------------------
+ * Sigmoid routing with an expert-selection bias (Sec. 4.1: DeepSeek-V3.1 and GLM-5.2,
+ * routed scaling factor 2.5).  Each expert's affinity is the logistic function of its
+ * logit; the per-expert bias is added for ranking only; the selected affinities are
+ * normalised over the selection and scaled.
+ * ------------------------------------------------------------------------------- */
+void mo_select_sigmoid(int T, int E, int k, const double* logits, const float* sel_bias, double scale,
+                       int32_t* ids, double* w)
+{
+    int t, j, e;
+    char* taken = (char*)malloc((size_t)E);
+    double* a = (double*)malloc(sizeof(double) * (size_t)E);
+    double* score = (double*)malloc(sizeof(double) * (size_t)E);
+    for (t = 0; t < T; ++t) {
+        double sum = 0.0;
+        for (e = 0; e < E; ++e) {
+            a[e] = 1.0 / (1.0 + exp(-logits[(size_t)t * E + e]));
+            score[e] = a[e] + (sel_bias ? (double)sel_bias[e] : 0.0);
+        }
+        memset(taken, 0, (size_t)E);
+        for (j = 0; j < k; ++j) {
+            int best = -1;
+            for (e = 0; e < E; ++e) {
+                if (taken[e]) continue;
+                if (best < 0 || score[e] > score[best]) best = e;
+            }
+            taken[best] = 1;
+            ids[(size_t)t * k + j] = best;
+            sum += a[best];
+        }
+        for (j = 0; j < k; ++j) w[(size_t)t * k + j] = scale * a[ids[(size_t)t * k + j]] / sum;
+    }
+    free(taken);
+    free(a);
+    free(score);
+}
+
+/* ---------------------------------------------------------------------------------
  * The operator.
  * ------------------------------------------------------------------------------- */
 static double silu(double g) { return g / (1.0 + exp(-g)); }
@@ -168,6 +205,17 @@ int mo_forward(int T, int H, int E, int I, int k, int renorm,
                const uint8_t* const* w2, const float* const* w2s,
                const int32_t* ids_in, const double* w_in,
                double* ref, mo_debug_t* dbg)
+{
+    return mo_forward_policy(T, H, E, I, k, renorm, MO_ROUTING_SOFTMAX, NULL, 1.0, x_bf16, rw_bf16, bias,
+                             w13, w13s, w2, w2s, ids_in, w_in, ref, dbg);
+}
+
+int mo_forward_policy(int T, int H, int E, int I, int k, int renorm, int policy, const float* sel_bias,
+                      double scale, const uint16_t* x_bf16, const uint16_t* rw_bf16, const float* bias,
+                      const uint8_t* const* w13, const float* const* w13s,
+                      const uint8_t* const* w2, const float* const* w2s,
+                      const int32_t* ids_in, const double* w_in,
+                      double* ref, mo_debug_t* dbg)
 {
     const int HB = H / 128, IB = I / 128;
     int t, j, g, n, kb, kk, i, hh;
@@ -184,6 +232,13 @@ int mo_forward(int T, int H, int E, int I, int k, int renorm,
     if (T < 0 || H <= 0 || I <= 0 || E <= 0 || H % 128 || I % 128) return -1;
     if (k < 1 || k > E) return -1;
     if ((ids_in == NULL) != (w_in == NULL)) return -1;
+    if (policy == MO_ROUTING_SOFTMAX) {
+        if (sel_bias || scale != 1.0) return -1;
+    } else if (policy == MO_ROUTING_SIGMOID_BIAS) {
+        if (!(scale > 0.0)) return -1;
+    } else {
+        return -1;
+    }
     if (T == 0) return 0;
 
     for (n = 0; n < 256; ++n) dec[n] = mo_e4m3_decode((uint8_t)n);
@@ -199,14 +254,15 @@ int mo_forward(int T, int H, int E, int I, int k, int renorm,
     y = (double*)malloc(sizeof(double) * (size_t)H);
     tmp = (float*)malloc(sizeof(float) * 128);
 
-    /* 1. routing: logits, softmax, top-k (or the injected selection) */
+    /* 1. routing: logits, softmax or sigmoid selection, top-k (or the injected selection) */
     if (ids_in) {
         memcpy(ids, ids_in, sizeof(int32_t) * (size_t)T * k);
         memcpy(wts, w_in, sizeof(double) * (size_t)T * k);
     } else {
         double* logits = (double*)malloc(sizeof(double) * (size_t)T * E);
         mo_router_logits(T, H, E, x_bf16, rw_bf16, bias, logits);
-        mo_select(T, E, k, renorm, logits, ids, wts);
+        if (policy == MO_ROUTING_SOFTMAX) mo_select(T, E, k, renorm, logits, ids, wts);
+        else mo_select_sigmoid(T, E, k, logits, sel_bias, scale, ids, wts);
         free(logits);
     }
     for (t = 0; t < T * k; ++t) {

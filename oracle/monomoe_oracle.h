@@ -8,7 +8,8 @@
  * generator with it, and must fail loudly rather than fall back to it.
  *
  * What is computed (paper Sec. 3 "MonoMoE Design" and Sec. 4.1 "Experimental Setup"):
- * router logits, softmax + top-k selection, per-token per-128-element dynamic E4M3
+ * router logits, softmax + top-k selection (or sigmoid + selection bias), per-token
+ * per-128-element dynamic E4M3
  * activation quantisation, the block-FP8 gate/up projection with 128x128 fp32 weight
  * block scales, SiLU(gate)*up, requantisation, the block-FP8 down projection and the
  * top-k weighted reduction.  The weight-major schedule of the paper changes when and
@@ -60,6 +61,18 @@ void mo_router_logits(int T, int H, int E, const uint16_t* x_bf16, const uint16_
  * w_j = p_{id_j} / sum_j' p_{id_j'}, otherwise w_j = p_{id_j}. */
 void mo_select(int T, int E, int k, int renorm, const double* logits, int32_t* ids, double* w);
 
+/* Sigmoid routing with an expert-selection bias and a routed scaling factor (Sec. 4.1:
+ * the DeepSeek-V3.1 and GLM-5.2 shapes, scaling factor 2.5; the formulas are those of the
+ * cited DeepSeek-V3 report): affinity a_e = 1 / (1 + exp(-logit_e)); experts are ranked by
+ * a_e + sel_bias[e] (sel_bias may be NULL = 0), descending, equal scores ranked by lower
+ * expert index; the bias steers the selection only:
+ *   w_j = scale * a_{id_j} / sum_j' a_{id_j'}. */
+void mo_select_sigmoid(int T, int E, int k, const double* logits, const float* sel_bias, double scale,
+                       int32_t* ids, double* w);
+
+/* Routing policies of mo_forward_policy. */
+enum { MO_ROUTING_SOFTMAX = 0, MO_ROUTING_SIGMOID_BIAS = 1 };
+
 /* Optional intermediate outputs of mo_forward; any pointer may be NULL.
  * Pair index p = t*k + j (token t, j-th selected expert). */
 typedef struct {
@@ -90,6 +103,17 @@ int mo_forward(int T, int H, int E, int I, int k, int renorm,
                const uint8_t* const* w2, const float* const* w2s,
                const int32_t* ids_in, const double* w_in,
                double* ref, mo_debug_t* dbg);
+
+/* mo_forward with the routing policy made explicit: MO_ROUTING_SOFTMAX (renorm as in
+ * mo_select; sel_bias must be NULL and scale 1) or MO_ROUTING_SIGMOID_BIAS (mo_select_sigmoid
+ * with sel_bias and scale; renorm is ignored).  bias, when set, is added to the logits under
+ * either policy. */
+int mo_forward_policy(int T, int H, int E, int I, int k, int renorm, int policy, const float* sel_bias,
+                      double scale, const uint16_t* x_bf16, const uint16_t* rw_bf16, const float* bias,
+                      const uint8_t* const* w13, const float* const* w13s,
+                      const uint8_t* const* w2, const float* const* w2s,
+                      const int32_t* ids_in, const double* w_in,
+                      double* ref, mo_debug_t* dbg);
 
 #ifdef __cplusplus
 }

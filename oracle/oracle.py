@@ -33,6 +33,11 @@ def lib():
         L.mo_select.argtypes = [ctypes.c_int] * 4 + [ctypes.c_void_p] * 3
         L.mo_forward.restype = ctypes.c_int
         L.mo_forward.argtypes = [ctypes.c_int] * 6 + [ctypes.c_void_p] * 11
+        L.mo_select_sigmoid.restype = None
+        L.mo_select_sigmoid.argtypes = [ctypes.c_int] * 3 + [ctypes.c_void_p] * 2 + [ctypes.c_double] + \
+            [ctypes.c_void_p] * 2
+        L.mo_forward_policy.restype = ctypes.c_int
+        L.mo_forward_policy.argtypes = [ctypes.c_int] * 7 + [ctypes.c_void_p, ctypes.c_double] + [ctypes.c_void_p] * 11
         _lib = L
     return _lib
 
@@ -87,12 +92,26 @@ def select(logits, k, renorm):
     return ids, w
 
 
+SOFTMAX, SIGMOID_BIAS = 0, 1
+
+
+def select_sigmoid(logits, k, sel_bias=None, scale=2.5):
+    logits = np.ascontiguousarray(logits, dtype=np.float64)
+    T, E = logits.shape
+    b = None if sel_bias is None else np.ascontiguousarray(sel_bias, dtype=np.float32)
+    ids = np.zeros((T, k), dtype=np.int32)
+    w = np.zeros((T, k), dtype=np.float64)
+    lib().mo_select_sigmoid(T, E, k, _p(logits), _p(b), float(scale), _p(ids), _p(w))
+    return ids, w
+
+
 def forward(x_bf16, rw_bf16, w13, w13s, w2, w2s, k, renorm, bias=None, ids_in=None, w_in=None,
-            debug=False, experts=None):
+            debug=False, experts=None, policy=SOFTMAX, sel_bias=None, scale=1.0):
     """The whole operator.
 
     x_bf16 uint16 [T,H]; rw_bf16 uint16 [E,H]; w13 uint8 [E,2I,H] (or a dict expert ->
     [2I,H] array); w13s float32 [E,2I/128,H/128] (or dict); w2 / w2s likewise.
+    policy SOFTMAX (renorm as given) or SIGMOID_BIAS (sel_bias float32 [E] or None, scale).
     Returns ref float64 [T,H] and, with debug=True, a dict of intermediates.
     """
     x = np.ascontiguousarray(x_bf16, dtype=np.uint16)
@@ -139,7 +158,9 @@ def forward(x_bf16, rw_bf16, w13, w13s, w2, w2s, k, renorm, bias=None, ids_in=No
         }
         dbg = _Debug(_p(d["ids"]), _p(d["w"]), _p(d["xq"]), _p(d["xs"]), _p(d["h"]), _p(d["act"]),
                      _p(d["aq"]), _p(d["as"]), _p(d["y"]))
-    rc = lib().mo_forward(T, H, E, I, k, int(bool(renorm)), _p(x), _p(rw), _p(b),
+    sb = None if sel_bias is None else np.ascontiguousarray(sel_bias, dtype=np.float32)
+    rc = lib().mo_forward_policy(T, H, E, I, k, int(bool(renorm)), int(policy), _p(sb), float(scale),
+                          _p(x), _p(rw), _p(b),
                           ctypes.cast(t13, ctypes.c_void_p), ctypes.cast(t13s, ctypes.c_void_p),
                           ctypes.cast(t2, ctypes.c_void_p), ctypes.cast(t2s, ctypes.c_void_p),
                           _p(ii), _p(wi), _p(ref), ctypes.byref(dbg) if dbg is not None else None)

@@ -216,3 +216,32 @@ def test_cosine_against_float_reference(orc, dist, name, T):
     unq = float_reference(inp, d["ids"], d["w"])
     cos = float(np.sum(ref * unq) / np.sqrt(np.sum(ref ** 2) * np.sum(unq ** 2)))
     assert cos >= 0.998, cos
+
+
+def test_sigmoid_policy_equals_injected_sigmoid_selection(orc):
+    # the sigmoid-routed operator is the operator with the sigmoid selection injected: the
+    # selection is computed from the same fp64 logits, and the expert path is shared
+    c = tiny_inputs(T=3, seed=7)
+    E = c["w13"].shape[0]
+    sel_bias = (np.random.default_rng(7).standard_normal(E) * 0.2).astype(np.float32)
+    ref, d = orc.forward(c["x"], c["rw"], c["w13"], c["w13s"], c["w2"], c["w2s"], 2, True, debug=True,
+                         policy=orc.SIGMOID_BIAS, sel_bias=sel_bias, scale=2.5)
+    ids, w = orc.select_sigmoid(orc.router_logits(c["x"], c["rw"]), 2, sel_bias, 2.5)
+    assert np.array_equal(d["ids"], ids)
+    np.testing.assert_array_equal(d["w"], w)
+    inj = orc.forward(c["x"], c["rw"], c["w13"], c["w13s"], c["w2"], c["w2s"], 2, True, ids_in=ids, w_in=w)
+    np.testing.assert_array_equal(ref, inj)
+    np.testing.assert_allclose(d["w"].sum(axis=1), 2.5, rtol=1e-13)
+
+
+def test_policy_arguments_are_checked(orc):
+    c = tiny_inputs(T=1)
+    args = (c["x"], c["rw"], c["w13"], c["w13s"], c["w2"], c["w2s"], 2, True)
+    with pytest.raises(ValueError):   # softmax takes no selection bias
+        orc.forward(*args, policy=orc.SOFTMAX, sel_bias=np.zeros(c["w13"].shape[0], np.float32))
+    with pytest.raises(ValueError):   # nor a scaling factor
+        orc.forward(*args, policy=orc.SOFTMAX, scale=2.5)
+    with pytest.raises(ValueError):
+        orc.forward(*args, policy=orc.SIGMOID_BIAS, scale=0.0)
+    with pytest.raises(ValueError):
+        orc.forward(*args, policy=7)

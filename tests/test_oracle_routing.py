@@ -90,3 +90,60 @@ def test_weight_ratios_follow_logit_gaps(orc):
             for j in range(1, 8):
                 r = w[t, 0] / w[t, j]
                 assert abs(r / np.exp(logits[t, ids[t, 0]] - logits[t, ids[t, j]]) - 1) < 1e-12
+
+
+# ---- sigmoid routing with an expert-selection bias and a routed scaling factor ----
+# Independent references: scipy's logistic function (expit), brute-force sorting, and
+# relations that hold whatever the implementation.
+from scipy.special import expit
+
+
+def test_sigmoid_select_matches_brute_force_and_expit(orc):
+    rng = np.random.default_rng(21)
+    for trial in range(40):
+        T, E = int(rng.integers(1, 6)), int(rng.integers(2, 40))
+        k = int(rng.integers(1, E + 1))
+        logits = rng.standard_normal((T, E))
+        bias = (rng.standard_normal(E) * 0.3).astype(np.float32)
+        if trial % 3 == 0:   # exact score ties: equal logits and equal biases
+            logits = np.round(logits)
+            bias = np.round(bias * 2).astype(np.float32) / 2
+        scale = float(rng.choice([1.0, 2.5]))
+        ids, w = orc.select_sigmoid(logits, k, bias, scale)
+        for t in range(T):
+            a = expit(logits[t])
+            score = a + bias.astype(np.float64)
+            assert ids[t].tolist() == brute_topk(score.tolist(), k)
+            sel = a[ids[t]]
+            np.testing.assert_allclose(w[t], scale * sel / sel.sum(), rtol=1e-13)
+            assert abs(w[t].sum() - scale) < 1e-12
+
+
+def test_sigmoid_bias_steers_selection_not_weights(orc):
+    # a large bias on experts 3 and 7 forces them in; their weights still come from the
+    # unbiased affinities
+    rng = np.random.default_rng(22)
+    logits = rng.standard_normal((2, 16))
+    bias = np.zeros(16, np.float32)
+    bias[[3, 7]] = 10.0
+    ids, w = orc.select_sigmoid(logits, 4, bias, 2.5)
+    for t in range(2):
+        assert set(ids[t][:2].tolist()) == {3, 7}
+        a = expit(logits[t])
+        np.testing.assert_allclose(w[t], 2.5 * a[ids[t]] / a[ids[t]].sum(), rtol=1e-13)
+
+
+def test_sigmoid_without_bias_selects_like_softmax(orc):
+    # the logistic function is increasing, so with no bias it ranks experts as the logits do
+    rng = np.random.default_rng(23)
+    logits = rng.standard_normal((5, 64)) * 2
+    ids_s, _ = orc.select_sigmoid(logits, 8, None, 2.5)
+    ids_m, _ = orc.select(logits, 8, True)
+    assert np.array_equal(ids_s, ids_m)
+
+
+def test_sigmoid_equal_logits_gives_equal_scaled_weights(orc):
+    bias = np.arange(12, dtype=np.float32) * 0.01      # ranks experts 11, 10, 9, ...
+    ids, w = orc.select_sigmoid(np.full((1, 12), 0.3), 5, bias, 2.5)
+    assert ids[0].tolist() == [11, 10, 9, 8, 7]
+    np.testing.assert_allclose(w[0], 0.5, rtol=1e-15)
