@@ -74,6 +74,22 @@ void monomoe_plan_destroy(monomoe_plan_t plan);
  * selected experts and their weights.  The pointer is read by every later forward. */
 int monomoe_plan_set_router_bias(monomoe_plan_t plan, const float* bias);
 
+/* Routing policy (paper Sec. 4.1: softmax routing for the Qwen models; sigmoid routing
+ * with an expert-selection bias and a routed scaling factor of 2.5 for DeepSeek-V3.1 and
+ * GLM-5.2; Sec. 3.4 lists the policy p among the operator's runtime parameters).
+ *   MONOMOE_ROUTING_SOFTMAX (the default): top-k of the logits, softmax weights,
+ *     renormalised over the selection when the plan's renorm flag is set.  sel_bias must
+ *     be NULL and scale 1.
+ *   MONOMOE_ROUTING_SIGMOID_BIAS: affinity a_e = 1/(1+exp(-logit_e)); experts ranked by
+ *     a_e + sel_bias[e] (fp32 [E] device pointer, or NULL for none; lower index on ties);
+ *     w_j = scale * a_{e_j} / sum of the selected affinities (the renorm flag is ignored).
+ *     scale must be finite and > 0.
+ * A logit bias set with monomoe_plan_set_router_bias applies under either policy.  The
+ * sel_bias pointer is read by every later forward.  Returns MONOMOE_ERR_INVALID (plan
+ * unchanged) on a bad policy, scale, pointer alignment or a softmax bias/scale. */
+enum { MONOMOE_ROUTING_SOFTMAX = 0, MONOMOE_ROUTING_SIGMOID_BIAS = 1 };
+int monomoe_plan_set_routing(monomoe_plan_t plan, int policy, const float* sel_bias, float scale);
+
 /* The operator (paper Sec. 3.4 interface, Eq. 9 weight-major projections):
  *   x         bf16  [T,H]                 input token tile
  *   router_w  bf16  [E,H]                 logits = x . router_w^T (+ bias)

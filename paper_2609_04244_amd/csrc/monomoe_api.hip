@@ -4,6 +4,7 @@
 #include "monomoe_internal.h"
 
 #include <hip/hip_ext.h>
+#include <cmath>
 
 #include <new>
 #include <string.h>
@@ -25,6 +26,9 @@ struct monomoe_plan_s {
     int naq;
     int nslots;
     const float* bias;
+    const float* sel_bias;
+    int policy;
+    float route_scale;
     // workspace (one allocation)
     void* ws;
     size_t ws_bytes;
@@ -64,6 +68,9 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
     p.x = static_cast<const uint16_t*>(x);
     p.rw = static_cast<const uint16_t*>(router_w);
     p.bias = plan->bias;
+    p.sel_bias = plan->sel_bias;
+    p.policy = plan->policy;
+    p.route_scale = plan->route_scale;
     p.w13 = static_cast<const uint8_t*>(w13);
     p.w13s = w13_scale;
     p.w2 = static_cast<const uint8_t*>(w2);
@@ -150,6 +157,9 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     pl->renorm = renorm ? 1 : 0;
     pl->kern = kern;
     pl->bias = nullptr;
+    pl->sel_bias = nullptr;
+    pl->policy = MONOMOE_ROUTING_SOFTMAX;
+    pl->route_scale = 1.0f;
 
     int dev = 0;
     hipDeviceProp_t prop;
@@ -237,6 +247,24 @@ int monomoe_plan_set_router_bias(monomoe_plan_t plan, const float* bias) {
     if (!plan) return MONOMOE_ERR_INVALID;
     if (bias && !aligned16(bias)) return MONOMOE_ERR_INVALID;
     plan->bias = bias;
+    return MONOMOE_OK;
+}
+
+static_assert(MONOMOE_ROUTING_SOFTMAX == kRouteSoftmax && MONOMOE_ROUTING_SIGMOID_BIAS == kRouteSigmoidBias,
+              "routing policy values");
+int monomoe_plan_set_routing(monomoe_plan_t plan, int policy, const float* sel_bias, float scale) {
+    if (!plan) return MONOMOE_ERR_INVALID;
+    if (policy == MONOMOE_ROUTING_SOFTMAX) {
+        if (sel_bias || scale != 1.0f) return MONOMOE_ERR_INVALID;
+    } else if (policy == MONOMOE_ROUTING_SIGMOID_BIAS) {
+        if (!(scale > 0.0f) || !(scale < INFINITY)) return MONOMOE_ERR_INVALID;
+        if (sel_bias && !aligned16(sel_bias)) return MONOMOE_ERR_INVALID;
+    } else {
+        return MONOMOE_ERR_INVALID;
+    }
+    plan->policy = policy;
+    plan->sel_bias = sel_bias;
+    plan->route_scale = scale;
     return MONOMOE_OK;
 }
 

@@ -34,6 +34,9 @@ constexpr int ctl_words() { return kCtlEpoch + kGridMax; }
 
 enum : uint32_t { kDevOk = 0, kDevTimeout = 1, kDevBadIds = 2 };
 
+// Routing policies (the same values as MONOMOE_ROUTING_* of the C ABI).
+enum : int32_t { kRouteSoftmax = 0, kRouteSigmoidBias = 1 };
+
 // Phase stamps (test hook): per workgroup, s_memrealtime at these points.
 constexpr int kStamps = 24;
 enum : int {
@@ -45,7 +48,8 @@ struct KParams {
     // operator inputs/outputs (caller-owned)
     const uint16_t* x;        // bf16 [T,H]
     const uint16_t* rw;       // bf16 [E,H]
-    const float* bias;        // fp32 [E] or null
+    const float* bias;        // fp32 [E] logit bias or null
+    const float* sel_bias;    // fp32 [E] expert-selection bias (sigmoid routing) or null
     const uint8_t* w13;       // e4m3 [E,2I,H]
     const float* w13s;        // fp32 [E,2I/128,H/128]
     const uint8_t* w2;        // e4m3 [E,H,I]
@@ -72,6 +76,8 @@ struct KParams {
     int32_t fail_flag;
     // runtime shape and LDS layout
     int32_t T, E, k, renorm;
+    int32_t policy;           // MONOMOE_ROUTING_SOFTMAX / MONOMOE_ROUTING_SIGMOID_BIAS
+    float route_scale;        // routed scaling factor (sigmoid routing)
     int32_t naq;              // requantised-act LDS buffers (2 = double buffered, 1)
     int32_t nslots;           // partial-sum hand-off slots (power of two)
 };

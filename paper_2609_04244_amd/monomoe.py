@@ -18,10 +18,13 @@ MONOMOE_ERR_UNSUPPORTED = -2
 MONOMOE_ERR_OCCUPANCY = -3
 MONOMOE_ERR_HIP = -4
 MONOMOE_ERR_TIMEOUT = -5
+ROUTING_SOFTMAX = 0
+ROUTING_SIGMOID_BIAS = 1
 
 # Every symbol include/monomoe.h declares.
 EXPORTS = (
-    "monomoe_plan", "monomoe_plan_destroy", "monomoe_plan_set_router_bias", "monomoe_forward",
+    "monomoe_plan", "monomoe_plan_destroy", "monomoe_plan_set_router_bias", "monomoe_plan_set_routing",
+    "monomoe_forward",
     "monomoe_forward_debug", "monomoe_forward_timed", "monomoe_plan_status", "monomoe_plan_reset", "monomoe_plan_info",
     "monomoe_supported_shape", "monomoe_status_string", "monomoe_stream_copy", "monomoe_stream_read",
 )
@@ -69,6 +72,8 @@ def lib():
         L.monomoe_plan_destroy.restype = None
         L.monomoe_plan_set_router_bias.argtypes = [vp, vp]
         L.monomoe_plan_set_router_bias.restype = ctypes.c_int
+        L.monomoe_plan_set_routing.argtypes = [vp, ctypes.c_int, vp, ctypes.c_float]
+        L.monomoe_plan_set_routing.restype = ctypes.c_int
         L.monomoe_forward.argtypes = [vp] * 9
         L.monomoe_forward.restype = ctypes.c_int
         L.monomoe_forward_debug.argtypes = [vp] * 8 + [ctypes.POINTER(Debug), vp]
@@ -213,6 +218,14 @@ class Plan:
         rc = lib().monomoe_plan_set_router_bias(self._h, _ptr(bias))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_plan_set_router_bias")
+
+    def set_routing(self, policy, sel_bias=None, scale=1.0):
+        """ROUTING_SOFTMAX, or ROUTING_SIGMOID_BIAS with an fp32 [E] selection bias (or None)
+        and the routed scaling factor."""
+        rc = lib().monomoe_plan_set_routing(self._h, int(policy), _ptr(sel_bias), float(scale))
+        if rc != MONOMOE_OK:
+            raise MonoMoEError(rc, "monomoe_plan_set_routing")
+        self._sel_bias = sel_bias  # keep the tensor alive while the plan refers to it
 
     def info(self):
         inf = PlanInfo()

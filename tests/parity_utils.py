@@ -2,8 +2,9 @@
 run the oracle on the same bytes, and compare under the operator's correctness contract:
 
   * selected expert ids and the input quantisation (codes + scales) bit-exact, except
-    tokens whose oracle k-th and (k+1)-th logits differ by less than 1e-4: for those the
-    oracle's selection is injected and the token is counted separately;
+    tokens whose oracle k-th and (k+1)-th selection scores (logits; under sigmoid routing
+    logistic(logit) + selection bias) differ by less than 1e-4: for those the oracle's
+    selection is injected and the token is counted separately;
   * requantisation bit-exact when the GPU's own fp32 SiLU(gate)*up is fed to the
     oracle's quantiser;
   * output: max|out - ref| <= 2e-2 * rms(ref) and sum|out - ref| / sum|ref| <= 5e-3, where
@@ -43,11 +44,22 @@ def host_experts(inp, experts):
             {e: w2[i] for i, e in enumerate(ex)}, {e: w2s[i] for i, e in enumerate(ex)})
 
 
+def sigmoid_routed(inp):
+    return inp.get("policy", "softmax") == "sigmoid_bias"
+
+
 def oracle_routing(inp):
+    """The oracle's selection scores (the logits, or logistic(logit) + selection bias under
+    sigmoid routing; the near-tie rule applies to them), ids and weights."""
     x = wl.bf16_bits(inp["x"])
     rw = wl.bf16_bits(inp["router_w"])
     bias = None if inp["bias"] is None else inp["bias"].cpu().numpy()
     logits = oracle.router_logits(x, rw, bias)
+    if sigmoid_routed(inp):
+        sb = None if inp["sel_bias"] is None else inp["sel_bias"].cpu().numpy()
+        ids, w = oracle.select_sigmoid(logits, inp["k"], sb, inp["route_scale"])
+        scores = 1.0 / (1.0 + np.exp(-logits)) + (0.0 if sb is None else sb.astype(np.float64)[None, :])
+        return scores, ids, w
     ids, w = oracle.select(logits, inp["k"], inp["renorm"])
     return logits, ids, w
 
@@ -96,6 +108,8 @@ def run_case(inp, tokens=None, plan=None):
         plan = mm.Plan(T, H, E, I, k, renorm)
     if inp["bias"] is not None:
         plan.set_router_bias(inp["bias"])
+    if sigmoid_routed(inp):
+        plan.set_routing(mm.ROUTING_SIGMOID_BIAS, inp["sel_bias"], inp["route_scale"])
     logits, oids, ow = oracle_routing(inp)
     tie = near_tie_tokens(logits, k)
     g = _gpu(plan, inp)

@@ -35,7 +35,8 @@ def test_status_strings():
 
 
 def test_supported_shapes():
-    for H, I in ((256, 256), (2048, 768), (2048, 512), (7168, 2048), (4096, 14336), (7168, 256)):
+    for H, I in ((256, 256), (2048, 768), (2048, 512), (7168, 2048), (4096, 14336), (7168, 256), (3072, 1024),
+                 (6144, 256)):
         assert mm.supported_shape(H, I)
     assert not mm.supported_shape(2048, 1024)
     assert not mm.supported_shape(100, 256)
