@@ -34,6 +34,8 @@ struct monomoe_plan_s {
     size_t ws_bytes;
     uint32_t* ctl;
     uint64_t* logits;
+    uint64_t* xq;
+    uint64_t* xs;
     uint64_t* act;
     uint64_t* contrib;
 };
@@ -78,6 +80,8 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
     p.out = static_cast<uint16_t*>(out);
     p.ctl = plan->ctl;
     p.logits = plan->logits;
+    p.xqw = plan->xq;
+    p.xsw = plan->xs;
     p.act = plan->act;
     p.contrib = plan->contrib;
     p.spin_limit = kDefaultSpinTicks;
@@ -210,11 +214,13 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
         return MONOMOE_ERR_UNSUPPORTED;
     }
 
-    // workspace: control words | logits | act | contrib
+    // workspace: control words | logits | quantised input (codes, scales) | act | contrib
     const int T = Tl;
     size_t off = 0;
     const size_t o_ctl = off;    off = align_up(off + sizeof(uint32_t) * ctl_words(), 256);
     const size_t o_log = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * s.E, 256);
+    const size_t o_xq = off;     off = align_up(off + sizeof(uint64_t) * (size_t)T * s.H / 4, 256);
+    const size_t o_xs = off;     off = align_up(off + sizeof(uint64_t) * (size_t)T * s.H / 128, 256);
     const size_t o_act = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * topk * s.I, 256);
     const size_t o_out = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * topk * s.H, 256);
     pl->ws_bytes = off;
@@ -225,6 +231,8 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     uint8_t* base = static_cast<uint8_t*>(pl->ws);
     pl->ctl = reinterpret_cast<uint32_t*>(base + o_ctl);
     pl->logits = reinterpret_cast<uint64_t*>(base + o_log);
+    pl->xq = reinterpret_cast<uint64_t*>(base + o_xq);
+    pl->xs = reinterpret_cast<uint64_t*>(base + o_xs);
     pl->act = reinterpret_cast<uint64_t*>(base + o_act);
     pl->contrib = reinterpret_cast<uint64_t*>(base + o_out);
     const int zr = zero_workspace(pl);

@@ -58,6 +58,8 @@ struct KParams {
     // plan workspace
     uint32_t* ctl;            // control words
     uint64_t* logits;         // [T,E]   {fp32 logit, tag}
+    uint64_t* xqw;            // [T,H/4] {four E4M3 input codes, tag}
+    uint64_t* xsw;            // [T,H/128] {fp32 input scale, tag}
     uint64_t* act;            // [T*k,I] {fp32 SiLU(gate)*up, tag}
     uint64_t* contrib;        // [T*k,H] {fp32 routing-weighted expert output, tag}
     // test hooks (null when unused)
