@@ -174,9 +174,25 @@ typedef struct {
     int64_t workspace_bytes;
     int32_t scratch_bytes;   /* per-thread private (scratch) memory of the kernel: 0 when
                                 all of its state lives in registers and LDS            */
+    int32_t ring;            /* weight-ring depth of the current schedule             */
 } monomoe_plan_info_t;
 
 int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info);
+
+/* Schedule of a plan (paper Sec. 3.4: each shape's kernels are precompiled for a set of
+ * schedules and serving uses a fixed, offline-tuned one).  Here a schedule is
+ *   grid: persistent workgroups, 1 .. CUs x occupancy (0 = one per CU, the default);
+ *   ring: weight-prefetch depth in 256-deep tasks per compute wavefront, 2 or 4 (0 = the
+ *         shape's default).
+ * The task size and the per-expert workgroup groups follow from the weight-major partition
+ * and are not separate parameters.  Every schedule computes bit-identical outputs.  A new
+ * grid resets the plan's workspace (blocking; no launch of the plan may be pending).
+ * Returns MONOMOE_ERR_INVALID (plan unchanged) for an out-of-range grid or ring. */
+typedef struct {
+    int32_t grid;
+    int32_t ring;
+} monomoe_schedule_t;
+int monomoe_plan_set_schedule(monomoe_plan_t plan, const monomoe_schedule_t* sched);
 
 /* 1 if (H, I) is one of the compiled shapes, else 0. */
 int monomoe_supported_shape(int32_t H, int32_t I);

@@ -16,6 +16,7 @@ struct monomoe_plan_s {
     int topk;
     int renorm;
     const KernelEntry* kern;
+    const KernelVariant* var;   // the scheduled ring depth's kernel
     int device;
     int num_cus;
     int occupancy;
@@ -116,11 +117,11 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
     if (ev_start || ev_stop) {
         // the dispatch itself records the events (its begin and end), not the stream
         void* args[] = {&p};
-        if (hipExtLaunchKernel(plan->kern->fn, dim3(plan->grid), dim3(kThreads), args, (size_t)plan->lds_dyn, stream,
+        if (hipExtLaunchKernel(plan->var->fn, dim3(plan->grid), dim3(kThreads), args, (size_t)plan->lds_dyn, stream,
                                ev_start, ev_stop, 0) != hipSuccess)
             return MONOMOE_ERR_HIP;
     } else {
-        plan->kern->launch(p, plan->grid, (size_t)plan->lds_dyn, stream);
+        plan->var->launch(p, plan->grid, (size_t)plan->lds_dyn, stream);
     }
     if (hipGetLastError() != hipSuccess) return MONOMOE_ERR_HIP;
     return MONOMOE_OK;
@@ -160,6 +161,7 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     pl->topk = topk;
     pl->renorm = renorm ? 1 : 0;
     pl->kern = kern;
+    pl->var = &kern->v[kern->ring_default == kRings[0] ? 0 : 1];
     pl->bias = nullptr;
     pl->sel_bias = nullptr;
     pl->policy = MONOMOE_ROUTING_SOFTMAX;
@@ -174,7 +176,7 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     pl->device = dev;
     pl->num_cus = prop.multiProcessorCount;
     hipFuncAttributes attr;
-    if (hipFuncGetAttributes(&attr, kern->fn) != hipSuccess) {
+    if (hipFuncGetAttributes(&attr, pl->var->fn) != hipSuccess) {
         delete pl;
         return MONOMOE_ERR_HIP;
     }
@@ -194,20 +196,27 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
         delete pl;
         return MONOMOE_ERR_UNSUPPORTED;
     }
-    if (hipFuncSetAttribute(kern->fn, hipFuncAttributeMaxDynamicSharedMemorySize, pl->lds_dyn) != hipSuccess) {
-        delete pl;
-        return MONOMOE_ERR_HIP;
-    }
     int occ = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern->fn, kThreads, (size_t)pl->lds_dyn) != hipSuccess) {
-        delete pl;
-        return MONOMOE_ERR_HIP;
+    for (const KernelVariant& v : kern->v) {   // every depth must fit, so schedules can switch
+        hipFuncAttributes va;
+        int o = 0;
+        if (hipFuncGetAttributes(&va, v.fn) != hipSuccess ||
+            hipFuncSetAttribute(v.fn, hipFuncAttributeMaxDynamicSharedMemorySize, pl->lds_dyn) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, v.fn, kThreads, (size_t)pl->lds_dyn) != hipSuccess) {
+            delete pl;
+            return MONOMOE_ERR_HIP;
+        }
+        if ((int)va.sharedSizeBytes + pl->lds_dyn > (int)prop.sharedMemPerBlock) {
+            delete pl;
+            return MONOMOE_ERR_UNSUPPORTED;
+        }
+        if (&v == pl->var) occ = o;
+        if (o < 1) {
+            delete pl;
+            return MONOMOE_ERR_OCCUPANCY;
+        }
     }
     pl->occupancy = occ;
-    if (occ < 1) {
-        delete pl;
-        return MONOMOE_ERR_OCCUPANCY;
-    }
     pl->grid = pl->num_cus;   // one resident workgroup per CU
     if (pl->grid > kGridMax) {
         delete pl;
@@ -276,6 +285,28 @@ int monomoe_plan_set_routing(monomoe_plan_t plan, int policy, const float* sel_b
     return MONOMOE_OK;
 }
 
+int monomoe_plan_set_schedule(monomoe_plan_t plan, const monomoe_schedule_t* sched) {
+    if (!plan || !sched) return MONOMOE_ERR_INVALID;
+    const int grid = sched->grid == 0 ? plan->num_cus : sched->grid;
+    const int ring = sched->ring == 0 ? plan->kern->ring_default : sched->ring;
+    if (grid < 1 || grid > plan->num_cus * plan->occupancy || grid > kGridMax) return MONOMOE_ERR_INVALID;
+    const KernelVariant* var = nullptr;
+    for (const KernelVariant& v : plan->kern->v)
+        if (v.ring == ring) var = &v;
+    if (!var) return MONOMOE_ERR_INVALID;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return MONOMOE_ERR_INVALID;
+    // the launch epochs are per workgroup: a new grid starts from a clean workspace
+    if (grid != plan->grid) {
+        if (hipDeviceSynchronize() != hipSuccess) return MONOMOE_ERR_HIP;
+        const int zr = zero_workspace(plan);
+        if (zr != MONOMOE_OK) return zr;
+    }
+    plan->grid = grid;
+    plan->var = var;
+    return MONOMOE_OK;
+}
+
 int monomoe_forward(monomoe_plan_t plan, const void* x, const void* router_w, const void* w13,
                     const float* w13_scale, const void* w2, const float* w2_scale, void* out, hipStream_t stream) {
     return launch(plan, x, router_w, w13, w13_scale, w2, w2_scale, out, nullptr, stream);
@@ -318,7 +349,9 @@ int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info) {
     info->occupancy = plan->occupancy;
     info->num_cus = plan->num_cus;
     info->workspace_bytes = (int64_t)plan->ws_bytes;
-    info->scratch_bytes = plan->scratch;
+    hipFuncAttributes attr;
+    info->scratch_bytes = hipFuncGetAttributes(&attr, plan->var->fn) == hipSuccess ? (int32_t)attr.localSizeBytes : -1;
+    info->ring = plan->var->ring;
     return MONOMOE_OK;
 }
 

@@ -84,11 +84,17 @@ struct KParams {
     int32_t nslots;           // partial-sum hand-off slots (power of two)
 };
 
-// One compiled (H, I) specialisation.
-struct KernelEntry {
-    int H, I;
+// One compiled (H, I) specialisation, in every weight-ring depth of kRings.
+constexpr int kRings[2] = {2, 4};
+struct KernelVariant {
+    int ring;
     const void* fn;                                          // __global__ symbol
     void (*launch)(const KParams&, int grid, size_t lds, hipStream_t);
+};
+struct KernelEntry {
+    int H, I;
+    int ring_default;                                        // the shape's default depth
+    KernelVariant v[2];                                      // one per kRings entry
 };
 
 const KernelEntry* find_kernel(int H, int I);

@@ -24,6 +24,7 @@ ROUTING_SIGMOID_BIAS = 1
 # Every symbol include/monomoe.h declares.
 EXPORTS = (
     "monomoe_plan", "monomoe_plan_destroy", "monomoe_plan_set_router_bias", "monomoe_plan_set_routing",
+    "monomoe_plan_set_schedule",
     "monomoe_forward",
     "monomoe_forward_debug", "monomoe_forward_timed", "monomoe_plan_status", "monomoe_plan_reset", "monomoe_plan_info",
     "monomoe_supported_shape", "monomoe_status_string", "monomoe_stream_copy", "monomoe_stream_read",
@@ -52,7 +53,11 @@ class Debug(ctypes.Structure):
 class PlanInfo(ctypes.Structure):
     _fields_ = [("grid", ctypes.c_int32), ("block", ctypes.c_int32), ("lds_bytes", ctypes.c_int32),
                 ("occupancy", ctypes.c_int32), ("num_cus", ctypes.c_int32), ("workspace_bytes", ctypes.c_int64),
-                ("scratch_bytes", ctypes.c_int32)]
+                ("scratch_bytes", ctypes.c_int32), ("ring", ctypes.c_int32)]
+
+
+class Schedule(ctypes.Structure):
+    _fields_ = [("grid", ctypes.c_int32), ("ring", ctypes.c_int32)]
 
 
 _lib = None
@@ -74,6 +79,8 @@ def lib():
         L.monomoe_plan_set_router_bias.restype = ctypes.c_int
         L.monomoe_plan_set_routing.argtypes = [vp, ctypes.c_int, vp, ctypes.c_float]
         L.monomoe_plan_set_routing.restype = ctypes.c_int
+        L.monomoe_plan_set_schedule.argtypes = [vp, ctypes.POINTER(Schedule)]
+        L.monomoe_plan_set_schedule.restype = ctypes.c_int
         L.monomoe_forward.argtypes = [vp] * 9
         L.monomoe_forward.restype = ctypes.c_int
         L.monomoe_forward_debug.argtypes = [vp] * 8 + [ctypes.POINTER(Debug), vp]
@@ -226,6 +233,13 @@ class Plan:
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_plan_set_routing")
         self._sel_bias = sel_bias  # keep the tensor alive while the plan refers to it
+
+    def set_schedule(self, grid=0, ring=0):
+        """Persistent grid (0 = one workgroup per CU) and weight-ring depth (0 = default)."""
+        sch = Schedule(int(grid), int(ring))
+        rc = lib().monomoe_plan_set_schedule(self._h, ctypes.byref(sch))
+        if rc != MONOMOE_OK:
+            raise MonoMoEError(rc, "monomoe_plan_set_schedule")
 
     def info(self):
         inf = PlanInfo()
