@@ -38,7 +38,11 @@
 extern "C" {
 #endif
 
-/* T: tokens per decode step (0..16; T == 0 makes forward a no-op).
+/* T: tokens per decode step (0..64; T == 0 makes forward a no-op).  One launch processes
+ * a token tile of at most 16 (one MFMA N tile, and as many as the LDS staging of the
+ * shape holds: 8 for the 4096x14336 layer); a larger T runs as consecutive passes over
+ * token tiles, each streaming the weights of the experts that tile selects, so beyond one
+ * tile the operator is weight-major per pass, not across passes.
  * H: hidden size, I: expert intermediate size, both multiples of 128 from the set of
  * compiled shapes (monomoe_supported_shape()).  E: routed experts (1..512). */
 typedef struct {
@@ -50,7 +54,7 @@ typedef struct monomoe_plan_s* monomoe_plan_t;
 typedef enum {
     MONOMOE_OK = 0,
     MONOMOE_ERR_INVALID = -1,      /* bad argument: null/misaligned pointer, bad shape, bad topk */
-    MONOMOE_ERR_UNSUPPORTED = -2,  /* valid but not compiled: (H,I) pair, T > 16, E > 512     */
+    MONOMOE_ERR_UNSUPPORTED = -2,  /* valid but not compiled: (H,I) pair, T > 64, E > 512     */
     MONOMOE_ERR_OCCUPANCY = -3,    /* the persistent grid cannot be fully resident             */
     MONOMOE_ERR_HIP = -4,          /* a HIP runtime call failed                                */
     MONOMOE_ERR_TIMEOUT = -5       /* device: a bounded readiness wait expired                 */
@@ -116,7 +120,8 @@ int monomoe_forward(monomoe_plan_t plan, const void* x, const void* router_w,
  *   topk_ids_in / topk_w_in       [T,topk] replace the kernel's own selection (read);
  *                                 both or neither; ids distinct per token, in [0,E)
  *   stamps    u64   [grid,24]     per-workgroup s_memrealtime (100 MHz) stamps at phase
- *                                 boundaries, for latency breakdowns (written)
+ *                                 boundaries, for latency breakdowns (written; with
+ *                                 several token passes, those of the last pass)
  *   spin_limit_ticks              bound of every readiness wait in 100 MHz ticks
  *                                 (0 = the default of 2 s)
  *   fail_flag                     nonzero makes every workgroup wait on a condition that
@@ -147,7 +152,8 @@ int monomoe_forward_debug(monomoe_plan_t plan, const void* x, const void* router
 /* Measurement hook: monomoe_forward with the kernel launched through hipExtLaunchKernel,
  * so that `start` and `stop` (caller-created hipEvents, both non-NULL) take the dispatch's
  * own begin and end timestamps instead of the stream positions around it; the elapsed
- * time between them is the kernel duration that a kernel trace reports.  Same arguments,
+ * time between them is the kernel duration that a kernel trace reports (with several
+ * token passes: from the first pass's begin to the last pass's end).  Same arguments,
  * errors and asynchrony as monomoe_forward. */
 int monomoe_forward_timed(monomoe_plan_t plan, const void* x, const void* router_w,
                           const void* w13, const float* w13_scale,
@@ -175,6 +181,7 @@ typedef struct {
     int32_t scratch_bytes;   /* per-thread private (scratch) memory of the kernel: 0 when
                                 all of its state lives in registers and LDS            */
     int32_t ring;            /* weight-ring depth of the current schedule             */
+    int32_t tokens_per_pass; /* tokens one launch processes (T larger runs in passes) */
 } monomoe_plan_info_t;
 
 int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info);

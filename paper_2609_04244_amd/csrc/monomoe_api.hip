@@ -5,6 +5,7 @@
 
 #include <hip/hip_ext.h>
 #include <cmath>
+#include <algorithm>
 
 #include <new>
 #include <string.h>
@@ -26,6 +27,7 @@ struct monomoe_plan_s {
     int scratch;
     int naq;
     int nslots;
+    int tchunk;   // tokens per pass (T larger than one LDS-resident tile runs in passes)
     const float* bias;
     const float* sel_bias;
     int policy;
@@ -105,7 +107,6 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
         if (dbg->spin_limit_ticks) p.spin_limit = dbg->spin_limit_ticks;
         p.fail_flag = dbg->fail_flag;
     }
-    p.T = s.T;
     p.E = s.E;
     p.k = plan->topk;
     p.renorm = plan->renorm;
@@ -114,16 +115,37 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
 
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess || cur != plan->device) return MONOMOE_ERR_INVALID;
-    if (ev_start || ev_stop) {
-        // the dispatch itself records the events (its begin and end), not the stream
-        void* args[] = {&p};
-        if (hipExtLaunchKernel(plan->var->fn, dim3(plan->grid), dim3(kThreads), args, (size_t)plan->lds_dyn, stream,
-                               ev_start, ev_stop, 0) != hipSuccess)
-            return MONOMOE_ERR_HIP;
-    } else {
-        plan->var->launch(p, plan->grid, (size_t)plan->lds_dyn, stream);
+    // one launch per pass of at most tchunk tokens (one pass when T fits one tile); each
+    // pass sees its rows of every token-indexed buffer
+    const int K = plan->topk, H = s.H, I = s.I, tc = plan->tchunk;
+    for (int t0 = 0; t0 < s.T; t0 += tc) {
+        KParams q = p;
+        q.T = std::min(tc, s.T - t0);
+        q.x = p.x + (size_t)t0 * H;
+        q.out = p.out + (size_t)t0 * H;
+        if (p.d_ids) q.d_ids = p.d_ids + (size_t)t0 * K;
+        if (p.d_w) q.d_w = p.d_w + (size_t)t0 * K;
+        if (p.d_xq) q.d_xq = p.d_xq + (size_t)t0 * H;
+        if (p.d_xs) q.d_xs = p.d_xs + (size_t)t0 * (H / 128);
+        if (p.d_act) q.d_act = p.d_act + (size_t)t0 * K * I;
+        if (p.d_aq) q.d_aq = p.d_aq + (size_t)t0 * K * I;
+        if (p.d_as) q.d_as = p.d_as + (size_t)t0 * K * (I / 128);
+        if (p.d_out) q.d_out = p.d_out + (size_t)t0 * H;
+        if (p.inj_ids) q.inj_ids = p.inj_ids + (size_t)t0 * K;
+        if (p.inj_w) q.inj_w = p.inj_w + (size_t)t0 * K;
+        const bool first = t0 == 0, last = t0 + tc >= s.T;
+        if (ev_start || ev_stop) {
+            // the dispatch itself records the events (the first pass's begin, the last
+            // pass's end), not the stream
+            void* args[] = {&q};
+            if (hipExtLaunchKernel(plan->var->fn, dim3(plan->grid), dim3(kThreads), args, (size_t)plan->lds_dyn,
+                                   stream, first ? ev_start : nullptr, last ? ev_stop : nullptr, 0) != hipSuccess)
+                return MONOMOE_ERR_HIP;
+        } else {
+            plan->var->launch(q, plan->grid, (size_t)plan->lds_dyn, stream);
+        }
+        if (hipGetLastError() != hipSuccess) return MONOMOE_ERR_HIP;
     }
-    if (hipGetLastError() != hipSuccess) return MONOMOE_ERR_HIP;
     return MONOMOE_OK;
 }
 
@@ -151,7 +173,7 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     if (s.T < 0 || s.H <= 0 || s.I <= 0 || s.E <= 0) return MONOMOE_ERR_INVALID;
     if (s.H % 128 || s.I % 128) return MONOMOE_ERR_INVALID;
     if (topk < 1 || topk > s.E) return MONOMOE_ERR_INVALID;
-    if (s.T > kTMax || s.E > kEMax || topk > kKMax) return MONOMOE_ERR_UNSUPPORTED;
+    if (s.T > kTLimit || s.E > kEMax || topk > kKMax) return MONOMOE_ERR_UNSUPPORTED;
     const KernelEntry* kern = find_kernel(s.H, s.I);
     if (!kern) return MONOMOE_ERR_UNSUPPORTED;
 
@@ -185,8 +207,11 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     // double-buffer the requantised activation in LDS when it fits, else single-buffer;
     // then as many partial-sum slots as the rest of the LDS holds (more slots let the
     // compute wavefronts run further ahead of the helper's epilogues)
-    const int Tl = s.T > 0 ? s.T : 1;
+    // tokens per pass: the largest tile (<= kTMax, <= T) whose LDS footprint fits
     const int lds_cap = (int)prop.sharedMemPerBlock - pl->lds_static;
+    int Tl = std::min(std::max(s.T, 1), kTMax);
+    while (Tl > 1 && lds_dynamic_bytes(s.H, s.I, Tl, 1, kSlotsMin) > lds_cap) --Tl;
+    pl->tchunk = Tl;
     pl->naq = lds_dynamic_bytes(s.H, s.I, Tl, 2, kSlotsMin) <= lds_cap ? 2 : 1;
     pl->nslots = kSlotsMin;
     while (pl->nslots < kSlotsMax && lds_dynamic_bytes(s.H, s.I, Tl, pl->naq, pl->nslots * 2) <= lds_cap)
@@ -352,6 +377,7 @@ int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info) {
     hipFuncAttributes attr;
     info->scratch_bytes = hipFuncGetAttributes(&attr, plan->var->fn) == hipSuccess ? (int32_t)attr.localSizeBytes : -1;
     info->ring = plan->var->ring;
+    info->tokens_per_pass = plan->tchunk;
     return MONOMOE_OK;
 }
 

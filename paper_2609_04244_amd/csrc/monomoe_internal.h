@@ -10,7 +10,8 @@ namespace monomoe {
 constexpr int kComputeWaves = 4;              // wavefronts that stream weights and run MFMAs
 constexpr int kWaves = kComputeWaves + 1;     // + one helper wavefront (epilogues, flags)
 constexpr int kThreads = kWaves * 64;
-constexpr int kTMax = 16;                     // tokens per step: one 16-wide MFMA N tile
+constexpr int kTMax = 16;                     // tokens per pass: one 16-wide MFMA N tile
+constexpr int kTLimit = 64;                   // tokens per forward (larger T runs in passes)
 constexpr int kKMax = 16;                     // top-k bound
 constexpr int kEMax = 512;                    // experts bound (8 logits per lane in top-k)
 constexpr int kUMax = kTMax * kKMax;          // active experts bound (T*k, also <= E)

@@ -53,7 +53,7 @@ class Debug(ctypes.Structure):
 class PlanInfo(ctypes.Structure):
     _fields_ = [("grid", ctypes.c_int32), ("block", ctypes.c_int32), ("lds_bytes", ctypes.c_int32),
                 ("occupancy", ctypes.c_int32), ("num_cus", ctypes.c_int32), ("workspace_bytes", ctypes.c_int64),
-                ("scratch_bytes", ctypes.c_int32), ("ring", ctypes.c_int32)]
+                ("scratch_bytes", ctypes.c_int32), ("ring", ctypes.c_int32), ("tokens_per_pass", ctypes.c_int32)]
 
 
 class Schedule(ctypes.Structure):

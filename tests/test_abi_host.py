@@ -56,7 +56,7 @@ def _plan_rc(T, H, E, I, topk, renorm=1):
     ((1, 2048, 4, 768, 5), mm.MONOMOE_ERR_INVALID),         # topk > E
     ((-1, 2048, 128, 768, 8), mm.MONOMOE_ERR_INVALID),      # negative T
     ((1, 2048, 0, 768, 1), mm.MONOMOE_ERR_INVALID),         # no experts
-    ((17, 2048, 128, 768, 8), mm.MONOMOE_ERR_UNSUPPORTED),  # beyond one 16-wide token tile
+    ((65, 2048, 128, 768, 8), mm.MONOMOE_ERR_UNSUPPORTED),  # beyond 64 tokens per forward
     ((1, 2048, 600, 768, 8), mm.MONOMOE_ERR_UNSUPPORTED),   # E beyond 512
     ((1, 2048, 128, 768, 17), mm.MONOMOE_ERR_UNSUPPORTED),  # topk beyond 16
     ((1, 2048, 128, 1024, 8), mm.MONOMOE_ERR_UNSUPPORTED),  # (H, I) not compiled
