@@ -22,8 +22,9 @@
  *  - Entry points return MONOMOE_OK (0) or a negative monomoe_status_t.  An argument
  *    error enqueues nothing.
  *  - monomoe_forward() and monomoe_forward_debug() never synchronise, never allocate,
- *    and enqueue exactly one kernel on the given stream, so they can be captured into a
- *    HIP graph.  A plan owns device workspace: one plan must not be used by two launches
+ *    and enqueue one kernel on the given stream (consecutive kernels only for a schedule
+ *    that forces the single-tile kernel on more tokens than its tile, see
+ *    monomoe_plan_set_schedule), so they can be captured into a HIP graph.  A plan owns device workspace: one plan must not be used by two launches
  *    that can overlap (use one plan per stream).
  *  - The kernel reports failures it detects on the device (a bounded wait that expired)
  *    through a status word read with monomoe_plan_status().
@@ -38,11 +39,12 @@
 extern "C" {
 #endif
 
-/* T: tokens per decode step (0..64; T == 0 makes forward a no-op).  One launch processes
- * a token tile of at most 16 (one MFMA N tile, and as many as the LDS staging of the
- * shape holds: 8 for the 4096x14336 layer); a larger T runs as consecutive passes over
- * token tiles, each streaming the weights of the experts that tile selects, so beyond one
- * tile the operator is weight-major per pass, not across passes.
+/* T: tokens per decode step (0..64; T == 0 makes forward a no-op).  Up to one MFMA N
+ * tile of tokens (16, or as many as the LDS staging of the shape holds: 9 for the
+ * 4096x14336 layer) the single-tile kernel runs; beyond that the multi-tile kernel, which
+ * compacts each active expert's tokens into segments of up to R tokens (R from the LDS
+ * budget, see monomoe_plan_info) on several N tiles, so the weights of an expert are read
+ * once per forward unless more than R tokens select it.  Either way one launch.
  * H: hidden size, I: expert intermediate size, both multiples of 128 from the set of
  * compiled shapes (monomoe_supported_shape()).  E: routed experts (1..512). */
 typedef struct {
@@ -121,7 +123,7 @@ int monomoe_forward(monomoe_plan_t plan, const void* x, const void* router_w,
  *                                 both or neither; ids distinct per token, in [0,E)
  *   stamps    u64   [grid,24]     per-workgroup s_memrealtime (100 MHz) stamps at phase
  *                                 boundaries, for latency breakdowns (written; with
- *                                 several token passes, those of the last pass)
+ *                                 several single-tile passes, those of the last pass)
  *   spin_limit_ticks              bound of every readiness wait in 100 MHz ticks
  *                                 (0 = the default of 2 s)
  *   fail_flag                     nonzero makes every workgroup wait on a condition that
@@ -182,6 +184,9 @@ typedef struct {
                                 all of its state lives in registers and LDS            */
     int32_t ring;            /* weight-ring depth of the current schedule             */
     int32_t tokens_per_pass; /* tokens one launch processes (T larger runs in passes) */
+    int32_t multi_tile;      /* 1 when the multi-tile kernel runs, else 0             */
+    int32_t group_tokens;    /* multi-tile: R, the most tokens of one expert segment  */
+    int32_t down_slices;     /* multi-tile: K slices of the down projection           */
 } monomoe_plan_info_t;
 
 int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info);
@@ -190,14 +195,24 @@ int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info);
  * schedules and serving uses a fixed, offline-tuned one).  Here a schedule is
  *   grid: persistent workgroups, 1 .. CUs x occupancy (0 = one per CU, the default);
  *   ring: weight-prefetch depth in 256-deep tasks per compute wavefront, 2 or 4 (0 = the
- *         shape's default).
+ *         shape's default); the multi-tile kernel has depth 2 only;
+ *   kernel: MONOMOE_KERNEL_AUTO (0: single-tile up to its tile, multi-tile beyond),
+ *         MONOMOE_KERNEL_SINGLE (token passes of one tile each beyond it) or
+ *         MONOMOE_KERNEL_MULTI (also below one tile);
+ *   group_tokens: multi-tile only, a cap on R (0 = the largest the LDS holds), e.g. to
+ *         study segment splitting.
  * The task size and the per-expert workgroup groups follow from the weight-major partition
- * and are not separate parameters.  Every schedule computes bit-identical outputs.  A new
- * grid resets the plan's workspace (blocking; no launch of the plan may be pending).
- * Returns MONOMOE_ERR_INVALID (plan unchanged) for an out-of-range grid or ring. */
+ * and are not separate parameters.  Schedules that differ only in grid or ring compute
+ * bit-identical outputs; the kernel choice and R change the order of fp32 summation only.
+ * A new grid resets the plan's workspace (blocking; no launch of the plan may be pending).
+ * Returns MONOMOE_ERR_INVALID (plan unchanged) for an out-of-range field, and
+ * MONOMOE_ERR_UNSUPPORTED when the requested kernel cannot hold the shape's tiles. */
+enum { MONOMOE_KERNEL_AUTO = 0, MONOMOE_KERNEL_SINGLE = 1, MONOMOE_KERNEL_MULTI = 2 };
 typedef struct {
     int32_t grid;
     int32_t ring;
+    int32_t kernel;
+    int32_t group_tokens;
 } monomoe_schedule_t;
 int monomoe_plan_set_schedule(monomoe_plan_t plan, const monomoe_schedule_t* sched);
 

@@ -12,14 +12,29 @@
 
 using namespace monomoe;
 
+// Kernel choice and LDS layout of a plan.
+struct KernelConfig {
+    const KernelVariant* var;   // the kernel that runs
+    int mt;                     // 1: multi-tile kernel
+    int occupancy;
+    int lds_dyn;
+    int lds_static;
+    int naq;
+    int nslots;
+    int tchunk;                 // single-tile: tokens per pass (T beyond one tile runs in passes)
+    int rows, pool, tiles;      // multi-tile: R, quantised-input ring rows, N tiles per slot
+};
+
 struct monomoe_plan_s {
     monomoe_shape_t shape;
     int topk;
     int renorm;
     const KernelEntry* kern;
-    const KernelVariant* var;   // the scheduled ring depth's kernel
+    const KernelVariant* mtv;   // the shape's multi-tile kernel
+    const KernelVariant* var;   // the kernel that runs (scheduled ring depth, or multi-tile)
     int device;
     int num_cus;
+    int lds_total;              // LDS per workgroup of the device
     int occupancy;
     int grid;
     int lds_dyn;
@@ -28,6 +43,8 @@ struct monomoe_plan_s {
     int naq;
     int nslots;
     int tchunk;   // tokens per pass (T larger than one LDS-resident tile runs in passes)
+    int mt;       // multi-tile kernel
+    int mt_rows, mt_pool, mt_tiles;
     const float* bias;
     const float* sel_bias;
     int policy;
@@ -50,6 +67,117 @@ constexpr uint64_t kDefaultSpinTicks = 200000000ull;   // 2 s of the 100 MHz rea
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Single-tile kernel at ring depth `ring`: the largest token tile (<= kTMax, <= T) whose
+// LDS footprint fits, the requantised activation double-buffered when it fits, then as
+// many partial-sum slots as the rest of the LDS holds (more slots let the compute
+// wavefronts run further ahead of the helper's epilogues).  Every ring depth must fit, so
+// schedules can switch.
+int config_single(const monomoe_plan_s* pl, int ring, KernelConfig* c) {
+    const monomoe_shape_t& s = pl->shape;
+    const KernelVariant* var = nullptr;
+    for (const KernelVariant& v : pl->kern->v)
+        if (v.ring == ring) var = &v;
+    if (!var) return MONOMOE_ERR_INVALID;
+    hipFuncAttributes attr;
+    if (hipFuncGetAttributes(&attr, var->fn) != hipSuccess) return MONOMOE_ERR_HIP;
+    KernelConfig k{};
+    k.var = var;
+    k.lds_static = (int)attr.sharedSizeBytes;
+    const int lds_cap = pl->lds_total - k.lds_static;
+    int Tl = std::min(std::max(s.T, 1), kTMax);
+    while (Tl > 1 && lds_dynamic_bytes(s.H, s.I, Tl, 1, kSlotsMin) > lds_cap) --Tl;
+    k.tchunk = Tl;
+    k.naq = lds_dynamic_bytes(s.H, s.I, Tl, 2, kSlotsMin) <= lds_cap ? 2 : 1;
+    k.nslots = kSlotsMin;
+    while (k.nslots < kSlotsMax && lds_dynamic_bytes(s.H, s.I, Tl, k.naq, k.nslots * 2) <= lds_cap) k.nslots *= 2;
+    k.lds_dyn = lds_dynamic_bytes(s.H, s.I, Tl, k.naq, k.nslots);
+    if (k.lds_dyn > lds_cap) return MONOMOE_ERR_UNSUPPORTED;
+    for (const KernelVariant& v : pl->kern->v) {
+        hipFuncAttributes va;
+        int o = 0;
+        if (hipFuncGetAttributes(&va, v.fn) != hipSuccess ||
+            hipFuncSetAttribute(v.fn, hipFuncAttributeMaxDynamicSharedMemorySize, k.lds_dyn) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, v.fn, kThreads, (size_t)k.lds_dyn) != hipSuccess)
+            return MONOMOE_ERR_HIP;
+        if ((int)va.sharedSizeBytes + k.lds_dyn > pl->lds_total) return MONOMOE_ERR_UNSUPPORTED;
+        if (o < 1) return MONOMOE_ERR_OCCUPANCY;
+        if (&v == var) k.occupancy = o;
+    }
+    *c = k;
+    return MONOMOE_OK;
+}
+
+// Multi-tile kernel: the largest segment size R (<= T, <= group_cap when nonzero) whose
+// LDS layout fits, then as many quantised-input ring rows as the rest holds.  Segments
+// per forward are bounded by min(E, T*k) + ceil(T*k / R).
+int config_multi(const monomoe_plan_s* pl, int group_cap, KernelConfig* c) {
+    const monomoe_shape_t& s = pl->shape;
+    if (!pl->mtv) return MONOMOE_ERR_UNSUPPORTED;
+    hipFuncAttributes attr;
+    if (hipFuncGetAttributes(&attr, pl->mtv->fn) != hipSuccess) return MONOMOE_ERR_HIP;
+    KernelConfig k{};
+    k.var = pl->mtv;
+    k.mt = 1;
+    k.lds_static = (int)attr.sharedSizeBytes;
+    const int lds_cap = pl->lds_total - k.lds_static;
+    const int T = std::max(s.T, 1);
+    int R = std::min(T, kTLimit);
+    if (group_cap > 0) R = std::min(R, group_cap);
+    for (; R >= 1; --R) {
+        k.tiles = (R + 15) / 16;
+        if (mt_region_bytes(s.H, s.I, R, R) + mt_partials_bytes(kSlotsMin, k.tiles) <= lds_cap) break;
+    }
+    if (R < 1) return MONOMOE_ERR_UNSUPPORTED;
+    k.rows = R;
+    k.pool = R;
+    while (k.pool < 1024 && mt_region_bytes(s.H, s.I, k.pool + 1, R) + mt_partials_bytes(kSlotsMin, k.tiles) <= lds_cap)
+        ++k.pool;
+    const int pairs = T * pl->topk;
+    if (std::min(s.E, pairs) + (pairs + R - 1) / R > kQMax) return MONOMOE_ERR_UNSUPPORTED;
+    k.naq = 2;
+    k.nslots = kSlotsMin;
+    k.tchunk = T;
+    k.lds_dyn = mt_region_bytes(s.H, s.I, k.pool, R) + mt_partials_bytes(k.nslots, k.tiles);
+    int o = 0;
+    if (hipFuncSetAttribute(k.var->fn, hipFuncAttributeMaxDynamicSharedMemorySize, k.lds_dyn) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, k.var->fn, kThreads, (size_t)k.lds_dyn) != hipSuccess)
+        return MONOMOE_ERR_HIP;
+    if (o < 1) return MONOMOE_ERR_OCCUPANCY;
+    k.occupancy = o;
+    *c = k;
+    return MONOMOE_OK;
+}
+
+// Kernel for a request: MONOMOE_KERNEL_AUTO takes the single-tile kernel while T fits
+// its tile and the multi-tile kernel beyond (token passes if that cannot be configured).
+int configure(const monomoe_plan_s* pl, int kernel, int ring, int group_cap, KernelConfig* c) {
+    if (kernel == MONOMOE_KERNEL_MULTI) {
+        if (ring != 0 && ring != pl->mtv->ring) return MONOMOE_ERR_INVALID;
+        return config_multi(pl, group_cap, c);
+    }
+    const int r = ring == 0 ? pl->kern->ring_default : ring;
+    const int rc = config_single(pl, r, c);
+    if (rc != MONOMOE_OK || kernel == MONOMOE_KERNEL_SINGLE || pl->shape.T <= c->tchunk) return rc;
+    if (ring != 0 && ring != pl->mtv->ring) return MONOMOE_OK;   // that depth exists in the single-tile kernel only
+    KernelConfig m;
+    if (config_multi(pl, group_cap, &m) == MONOMOE_OK) *c = m;
+    return MONOMOE_OK;
+}
+
+void apply_config(monomoe_plan_s* pl, const KernelConfig& c) {
+    pl->var = c.var;
+    pl->mt = c.mt;
+    pl->occupancy = c.occupancy;
+    pl->lds_dyn = c.lds_dyn;
+    pl->lds_static = c.lds_static;
+    pl->naq = c.naq;
+    pl->nslots = c.nslots;
+    pl->tchunk = c.tchunk;
+    pl->mt_rows = c.rows;
+    pl->mt_pool = c.pool;
+    pl->mt_tiles = c.tiles;
+}
 
 int zero_workspace(monomoe_plan_s* pl) {
     if (hipMemset(pl->ws, 0, pl->ws_bytes) != hipSuccess) return MONOMOE_ERR_HIP;
@@ -112,12 +240,15 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
     p.renorm = plan->renorm;
     p.naq = plan->naq;
     p.nslots = plan->nslots;
+    p.mt_rows = (uint8_t)plan->mt_rows;
+    p.mt_tiles = (uint8_t)plan->mt_tiles;
+    p.mt_pool = (uint16_t)plan->mt_pool;
 
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess || cur != plan->device) return MONOMOE_ERR_INVALID;
     // one launch per pass of at most tchunk tokens (one pass when T fits one tile); each
     // pass sees its rows of every token-indexed buffer
-    const int K = plan->topk, H = s.H, I = s.I, tc = plan->tchunk;
+    const int K = plan->topk, H = s.H, I = s.I, tc = plan->mt ? s.T : plan->tchunk;
     for (int t0 = 0; t0 < s.T; t0 += tc) {
         KParams q = p;
         q.T = std::min(tc, s.T - t0);
@@ -183,7 +314,7 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     pl->topk = topk;
     pl->renorm = renorm ? 1 : 0;
     pl->kern = kern;
-    pl->var = &kern->v[kern->ring_default == kRings[0] ? 0 : 1];
+    pl->mtv = find_mt_kernel(s.H, s.I);
     pl->bias = nullptr;
     pl->sel_bias = nullptr;
     pl->policy = MONOMOE_ROUTING_SOFTMAX;
@@ -197,66 +328,39 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     }
     pl->device = dev;
     pl->num_cus = prop.multiProcessorCount;
-    hipFuncAttributes attr;
-    if (hipFuncGetAttributes(&attr, pl->var->fn) != hipSuccess) {
+    pl->lds_total = (int)prop.sharedMemPerBlock;
+    KernelConfig cfg;
+    const int cr = configure(pl, MONOMOE_KERNEL_AUTO, 0, 0, &cfg);
+    if (cr != MONOMOE_OK) {
         delete pl;
-        return MONOMOE_ERR_HIP;
+        return cr;
     }
-    pl->lds_static = (int)attr.sharedSizeBytes;
-    pl->scratch = (int)attr.localSizeBytes;
-    // double-buffer the requantised activation in LDS when it fits, else single-buffer;
-    // then as many partial-sum slots as the rest of the LDS holds (more slots let the
-    // compute wavefronts run further ahead of the helper's epilogues)
-    // tokens per pass: the largest tile (<= kTMax, <= T) whose LDS footprint fits
-    const int lds_cap = (int)prop.sharedMemPerBlock - pl->lds_static;
-    int Tl = std::min(std::max(s.T, 1), kTMax);
-    while (Tl > 1 && lds_dynamic_bytes(s.H, s.I, Tl, 1, kSlotsMin) > lds_cap) --Tl;
-    pl->tchunk = Tl;
-    pl->naq = lds_dynamic_bytes(s.H, s.I, Tl, 2, kSlotsMin) <= lds_cap ? 2 : 1;
-    pl->nslots = kSlotsMin;
-    while (pl->nslots < kSlotsMax && lds_dynamic_bytes(s.H, s.I, Tl, pl->naq, pl->nslots * 2) <= lds_cap)
-        pl->nslots *= 2;
-    pl->lds_dyn = lds_dynamic_bytes(s.H, s.I, Tl, pl->naq, pl->nslots);
-    if (pl->lds_dyn > lds_cap) {
-        delete pl;
-        return MONOMOE_ERR_UNSUPPORTED;
-    }
-    int occ = 0;
-    for (const KernelVariant& v : kern->v) {   // every depth must fit, so schedules can switch
-        hipFuncAttributes va;
-        int o = 0;
-        if (hipFuncGetAttributes(&va, v.fn) != hipSuccess ||
-            hipFuncSetAttribute(v.fn, hipFuncAttributeMaxDynamicSharedMemorySize, pl->lds_dyn) != hipSuccess ||
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, v.fn, kThreads, (size_t)pl->lds_dyn) != hipSuccess) {
+    apply_config(pl, cfg);
+    {
+        hipFuncAttributes attr;
+        if (hipFuncGetAttributes(&attr, pl->var->fn) != hipSuccess) {
             delete pl;
             return MONOMOE_ERR_HIP;
         }
-        if ((int)va.sharedSizeBytes + pl->lds_dyn > (int)prop.sharedMemPerBlock) {
-            delete pl;
-            return MONOMOE_ERR_UNSUPPORTED;
-        }
-        if (&v == pl->var) occ = o;
-        if (o < 1) {
-            delete pl;
-            return MONOMOE_ERR_OCCUPANCY;
-        }
+        pl->scratch = (int)attr.localSizeBytes;
     }
-    pl->occupancy = occ;
     pl->grid = pl->num_cus;   // one resident workgroup per CU
     if (pl->grid > kGridMax) {
         delete pl;
         return MONOMOE_ERR_UNSUPPORTED;
     }
 
-    // workspace: control words | logits | quantised input (codes, scales) | act | contrib
-    const int T = Tl;
+    // workspace: control words | logits | quantised input (codes, scales) | act | contrib,
+    // sized for one launch over every token and for the multi-tile kernel's down slices
+    const int T = std::max(s.T, 1);
+    const int nsl = (s.I / 128) / mt_slice_blocks(s.I / 128);
     size_t off = 0;
     const size_t o_ctl = off;    off = align_up(off + sizeof(uint32_t) * ctl_words(), 256);
     const size_t o_log = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * s.E, 256);
     const size_t o_xq = off;     off = align_up(off + sizeof(uint64_t) * (size_t)T * s.H / 4, 256);
     const size_t o_xs = off;     off = align_up(off + sizeof(uint64_t) * (size_t)T * s.H / 128, 256);
     const size_t o_act = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * topk * s.I, 256);
-    const size_t o_out = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * topk * s.H, 256);
+    const size_t o_out = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * topk * nsl * s.H, 256);
     pl->ws_bytes = off;
     if (hipMalloc(&pl->ws, pl->ws_bytes) != hipSuccess) {
         delete pl;
@@ -312,15 +416,16 @@ int monomoe_plan_set_routing(monomoe_plan_t plan, int policy, const float* sel_b
 
 int monomoe_plan_set_schedule(monomoe_plan_t plan, const monomoe_schedule_t* sched) {
     if (!plan || !sched) return MONOMOE_ERR_INVALID;
-    const int grid = sched->grid == 0 ? plan->num_cus : sched->grid;
-    const int ring = sched->ring == 0 ? plan->kern->ring_default : sched->ring;
-    if (grid < 1 || grid > plan->num_cus * plan->occupancy || grid > kGridMax) return MONOMOE_ERR_INVALID;
-    const KernelVariant* var = nullptr;
-    for (const KernelVariant& v : plan->kern->v)
-        if (v.ring == ring) var = &v;
-    if (!var) return MONOMOE_ERR_INVALID;
+    if (sched->kernel < MONOMOE_KERNEL_AUTO || sched->kernel > MONOMOE_KERNEL_MULTI) return MONOMOE_ERR_INVALID;
+    if (sched->group_tokens < 0 || sched->group_tokens > kTLimit) return MONOMOE_ERR_INVALID;
+    if (sched->ring != 0 && sched->ring != kRings[0] && sched->ring != kRings[1]) return MONOMOE_ERR_INVALID;
     int dev = -1;
     if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return MONOMOE_ERR_INVALID;
+    KernelConfig cfg;
+    const int cr = configure(plan, sched->kernel, sched->ring, sched->group_tokens, &cfg);
+    if (cr != MONOMOE_OK) return cr;
+    const int grid = sched->grid == 0 ? plan->num_cus : sched->grid;
+    if (grid < 1 || grid > plan->num_cus * cfg.occupancy || grid > kGridMax) return MONOMOE_ERR_INVALID;
     // the launch epochs are per workgroup: a new grid starts from a clean workspace
     if (grid != plan->grid) {
         if (hipDeviceSynchronize() != hipSuccess) return MONOMOE_ERR_HIP;
@@ -328,7 +433,7 @@ int monomoe_plan_set_schedule(monomoe_plan_t plan, const monomoe_schedule_t* sch
         if (zr != MONOMOE_OK) return zr;
     }
     plan->grid = grid;
-    plan->var = var;
+    apply_config(plan, cfg);
     return MONOMOE_OK;
 }
 
@@ -378,6 +483,9 @@ int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info) {
     info->scratch_bytes = hipFuncGetAttributes(&attr, plan->var->fn) == hipSuccess ? (int32_t)attr.localSizeBytes : -1;
     info->ring = plan->var->ring;
     info->tokens_per_pass = plan->tchunk;
+    info->multi_tile = plan->mt;
+    info->group_tokens = plan->mt ? plan->mt_rows : 0;
+    info->down_slices = plan->mt ? (plan->shape.I / 128) / mt_slice_blocks(plan->shape.I / 128) : 1;
     return MONOMOE_OK;
 }
 

@@ -1,5 +1,5 @@
 // Internal interface between the host runtime (monomoe_api.hip) and the persistent
-// kernel (monomoe_kernel.hip).  Not installed; not part of the C ABI.
+// kernels (monomoe_kernel.hip, monomoe_kernel_mt.hip).  Not installed; not part of the C ABI.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -20,6 +20,13 @@ constexpr int kSlotsMax = 32;                 //   a power of two in [min, max],
 
 constexpr int kGridMax = 1024;                // persistent workgroups at most
 
+// Multi-tile kernel (more tokens than one 16-wide N tile): tokens are compacted per
+// active expert and processed in segments of at most R tokens, each segment on up to
+// kNtMax N tiles.
+constexpr int kPMax = kTLimit * kKMax;        // token-expert pairs per forward
+constexpr int kNtMax = kTLimit / 16;          // N tiles per segment
+constexpr int kQMax = 640;                    // segments per forward
+
 // Control words at the head of the workspace (uint32 each).
 //  * status: sticky device status (kDev*).
 //  * epoch[wg]: launches this workgroup has completed.  All workgroups advance in
@@ -33,7 +40,7 @@ enum : int {
 };
 constexpr int ctl_words() { return kCtlEpoch + kGridMax; }
 
-enum : uint32_t { kDevOk = 0, kDevTimeout = 1, kDevBadIds = 2 };
+enum : uint32_t { kDevOk = 0, kDevTimeout = 1, kDevBadIds = 2, kDevOverflow = 3 };
 
 // Routing policies (the same values as MONOMOE_ROUTING_* of the C ABI).
 enum : int32_t { kRouteSoftmax = 0, kRouteSigmoidBias = 1 };
@@ -62,7 +69,8 @@ struct KParams {
     uint64_t* xqw;            // [T,H/4] {four E4M3 input codes, tag}
     uint64_t* xsw;            // [T,H/128] {fp32 input scale, tag}
     uint64_t* act;            // [T*k,I] {fp32 SiLU(gate)*up, tag}
-    uint64_t* contrib;        // [T*k,H] {fp32 routing-weighted expert output, tag}
+    uint64_t* contrib;        // [T*k,S,H] {fp32 routing-weighted expert output, tag}; S = 1,
+                              //   or the down projection's K slices (multi-tile kernel)
     // test hooks (null when unused)
     int32_t* d_ids;
     float* d_w;
@@ -83,7 +91,12 @@ struct KParams {
     float route_scale;        // routed scaling factor (sigmoid routing)
     int32_t naq;              // requantised-act LDS buffers (2 = double buffered, 1)
     int32_t nslots;           // partial-sum hand-off slots (power of two)
+    // multi-tile kernel only (packed into the struct's tail padding)
+    uint8_t mt_rows;          // R: tokens per segment at most (<= kTLimit)
+    uint8_t mt_tiles;         // N tiles per hand-off slot entry: ceil(R / 16)
+    uint16_t mt_pool;         // quantised-input LDS rows (>= R), used as a ring over segments
 };
+static_assert(sizeof(KParams) == 256, "kernel argument block");
 
 // One compiled (H, I) specialisation, in every weight-ring depth of kRings.
 constexpr int kRings[2] = {2, 4};
@@ -99,6 +112,7 @@ struct KernelEntry {
 };
 
 const KernelEntry* find_kernel(int H, int I);
+const KernelVariant* find_mt_kernel(int H, int I);           // the multi-tile kernel of a shape
 int kernel_count();
 const KernelEntry* kernel_at(int i);
 
@@ -122,5 +136,27 @@ __host__ __device__ inline int lds_partials_bytes(int nslots) { return nslots * 
 __host__ __device__ inline int lds_dynamic_bytes(int H, int I, int T, int naq, int nslots) {
     return lds_region_bytes(H, I, T, naq) + lds_partials_bytes(nslots);
 }
+
+// Multi-tile kernel LDS.  The down projection runs over K slices of DKB 128-deep blocks:
+// the largest even divisor of I/128 not above 16 (a slice of every segment's tokens is
+// what the requantised-act buffer holds).  Region: during gate/up a ring of `pool`
+// quantised-input rows plus their scale rows (and one zero scale row for absent token
+// columns); during down two requantised-act buffers of R rows of one slice (plus a zero
+// scale row).  Then the partial-sum slots, `tiles` 16x16 fp32 tiles per compute wavefront.
+__host__ __device__ constexpr int mt_slice_blocks(int IB) {
+    int d = IB < 16 ? IB : 16;
+    while (d > 2 && (IB % d != 0 || d % 2 != 0)) --d;
+    return d;
+}
+__host__ __device__ inline int mt_up_bytes(int H, int pool) { return pool * (H + 16) + (pool + 1) * (H / 128) * 4; }
+__host__ __device__ inline int mt_dn_buffer_bytes(int I, int R) {
+    const int dkb = mt_slice_blocks(I / 128);
+    return (R * (dkb * 128 + 16) + (R + 1) * dkb * 4 + 15) & ~15;
+}
+__host__ __device__ inline int mt_region_bytes(int H, int I, int pool, int R) {
+    const int up = mt_up_bytes(H, pool), dn = 2 * mt_dn_buffer_bytes(I, R);
+    return ((up > dn ? up : dn) + 15) & ~15;
+}
+__host__ __device__ inline int mt_partials_bytes(int nslots, int tiles) { return nslots * kComputeWaves * tiles * 64 * 16; }
 
 }  // namespace monomoe

@@ -20,6 +20,9 @@ MONOMOE_ERR_HIP = -4
 MONOMOE_ERR_TIMEOUT = -5
 ROUTING_SOFTMAX = 0
 ROUTING_SIGMOID_BIAS = 1
+KERNEL_AUTO = 0
+KERNEL_SINGLE = 1
+KERNEL_MULTI = 2
 
 # Every symbol include/monomoe.h declares.
 EXPORTS = (
@@ -53,11 +56,13 @@ class Debug(ctypes.Structure):
 class PlanInfo(ctypes.Structure):
     _fields_ = [("grid", ctypes.c_int32), ("block", ctypes.c_int32), ("lds_bytes", ctypes.c_int32),
                 ("occupancy", ctypes.c_int32), ("num_cus", ctypes.c_int32), ("workspace_bytes", ctypes.c_int64),
-                ("scratch_bytes", ctypes.c_int32), ("ring", ctypes.c_int32), ("tokens_per_pass", ctypes.c_int32)]
+                ("scratch_bytes", ctypes.c_int32), ("ring", ctypes.c_int32), ("tokens_per_pass", ctypes.c_int32),
+                ("multi_tile", ctypes.c_int32), ("group_tokens", ctypes.c_int32), ("down_slices", ctypes.c_int32)]
 
 
 class Schedule(ctypes.Structure):
-    _fields_ = [("grid", ctypes.c_int32), ("ring", ctypes.c_int32)]
+    _fields_ = [("grid", ctypes.c_int32), ("ring", ctypes.c_int32), ("kernel", ctypes.c_int32),
+                ("group_tokens", ctypes.c_int32)]
 
 
 _lib = None
@@ -234,9 +239,10 @@ class Plan:
             raise MonoMoEError(rc, "monomoe_plan_set_routing")
         self._sel_bias = sel_bias  # keep the tensor alive while the plan refers to it
 
-    def set_schedule(self, grid=0, ring=0):
-        """Persistent grid (0 = one workgroup per CU) and weight-ring depth (0 = default)."""
-        sch = Schedule(int(grid), int(ring))
+    def set_schedule(self, grid=0, ring=0, kernel=KERNEL_AUTO, group_tokens=0):
+        """Persistent grid (0 = one workgroup per CU), weight-ring depth (0 = default), kernel
+        (KERNEL_AUTO / KERNEL_SINGLE / KERNEL_MULTI) and the multi-tile segment cap (0 = none)."""
+        sch = Schedule(int(grid), int(ring), int(kernel), int(group_tokens))
         rc = lib().monomoe_plan_set_schedule(self._h, ctypes.byref(sch))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_plan_set_schedule")
