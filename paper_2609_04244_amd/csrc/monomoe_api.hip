@@ -151,6 +151,10 @@ int config_multi(const monomoe_plan_s* pl, int group_cap, KernelConfig* c) {
 
 // Kernel for a request: MONOMOE_KERNEL_AUTO takes the single-tile kernel while T fits
 // its tile and the multi-tile kernel beyond (token passes if that cannot be configured).
+// Where the down projection is sliced (I > 2048) the multi-tile kernel runs at every T:
+// the single-tile kernel requantises each expert's whole activation row (I = 14336) into
+// LDS before its first down task, which the sliced kernel splits over the slices
+// (measured: 85 vs 91 us at T = 1, 267 vs 343 us at T = 8 on the 4096x14336 layer).
 int configure(const monomoe_plan_s* pl, int kernel, int ring, int group_cap, KernelConfig* c) {
     if (kernel == MONOMOE_KERNEL_MULTI) {
         if (ring != 0 && ring != pl->mtv->ring) return MONOMOE_ERR_INVALID;
@@ -158,7 +162,9 @@ int configure(const monomoe_plan_s* pl, int kernel, int ring, int group_cap, Ker
     }
     const int r = ring == 0 ? pl->kern->ring_default : ring;
     const int rc = config_single(pl, r, c);
-    if (rc != MONOMOE_OK || kernel == MONOMOE_KERNEL_SINGLE || pl->shape.T <= c->tchunk) return rc;
+    const int ib = pl->shape.I / 128;
+    const bool sliced = mt_slice_blocks(ib) != ib;
+    if (rc != MONOMOE_OK || kernel == MONOMOE_KERNEL_SINGLE || (pl->shape.T <= c->tchunk && !sliced)) return rc;
     if (ring != 0 && ring != pl->mtv->ring) return MONOMOE_OK;   // that depth exists in the single-tile kernel only
     KernelConfig m;
     if (config_multi(pl, group_cap, &m) == MONOMOE_OK) *c = m;

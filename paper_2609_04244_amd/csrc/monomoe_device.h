@@ -671,53 +671,52 @@ __device__ __forceinline__ void router_rows(const KParams& p, int wg, int G, int
         __syncthreads();
     }
 }
-// The same for the token rows x[0..T) (a chunk of a larger input) into logits[0..T).
+// Router logits of one expert e for the token rows x[0..T) (a chunk of a larger input),
+// stored into logits[t*E + e]: the same arithmetic as router_rows.  All threads of the
+// workgroup take part.
 template <int H, int NT>
-__device__ __forceinline__ void router_rows_of(const KParams& p, const uint16_t* x, int T,
-                                               uint64_t* logits, int wg, int G, int tid, uint32_t tag, float* red) {
+__device__ __forceinline__ void router_row_of(const KParams& p, int e, const uint16_t* x, int T, uint64_t* logits,
+                                              int tid, uint32_t tag, float* red) {
     const int E = p.E;
     const int lane = tid & 63, wv = tid >> 6;
-    for (int e = wg; e < E; e += G) {
-        float acc_t[NT];
+    float acc_t[NT];
 #pragma unroll
-        for (int t = 0; t < NT; ++t) acc_t[t] = 0.0f;
-        const uint16_t* rrow = p.rw + (size_t)e * H;
-        for (int c = tid; c < H / 8; c += kThreads) {
-            // all loads first (token index clamped, so the count is fixed), then the FMAs
-            const uint4 rv = *reinterpret_cast<const uint4*>(rrow + c * 8);
-            uint4 xv[NT];
+    for (int t = 0; t < NT; ++t) acc_t[t] = 0.0f;
+    const uint16_t* rrow = p.rw + (size_t)e * H;
+    for (int c = tid; c < H / 8; c += kThreads) {
+        const uint4 rv = *reinterpret_cast<const uint4*>(rrow + c * 8);
+        uint4 xv[NT];
 #pragma unroll
-            for (int t = 0; t < NT; ++t)
-                xv[t] = *reinterpret_cast<const uint4*>(x + (size_t)min(t, T - 1) * H + c * 8);
-            const uint32_t rw4[4] = {rv.x, rv.y, rv.z, rv.w};
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                const uint32_t x4[4] = {xv[t].x, xv[t].y, xv[t].z, xv[t].w};
-                float a = acc_t[t];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    a = fmaf(bf16_to_f32(x4[q] & 0xFFFFu), bf16_to_f32(rw4[q] & 0xFFFFu), a);
-                    a = fmaf(bf16_to_f32(x4[q] >> 16), bf16_to_f32(rw4[q] >> 16), a);
-                }
-                acc_t[t] = a;
-            }
-        }
+        for (int t = 0; t < NT; ++t)
+            xv[t] = *reinterpret_cast<const uint4*>(x + (size_t)min(t, T - 1) * H + c * 8);
+        const uint32_t rw4[4] = {rv.x, rv.y, rv.z, rv.w};
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            if (t < T) {
-                const float s = wave_sum(acc_t[t]);
-                if (lane == 0) red[wv * kTMax + t] = s;
+            const uint32_t x4[4] = {xv[t].x, xv[t].y, xv[t].z, xv[t].w};
+            float a = acc_t[t];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                a = fmaf(bf16_to_f32(x4[q] & 0xFFFFu), bf16_to_f32(rw4[q] & 0xFFFFu), a);
+                a = fmaf(bf16_to_f32(x4[q] >> 16), bf16_to_f32(rw4[q] >> 16), a);
             }
+            acc_t[t] = a;
         }
-        __syncthreads();
-        if (tid < T) {
-            float s = 0.0f;
-            for (int v = 0; v < kWaves; ++v) s += red[v * kTMax + tid];
-            if (p.bias) s += p.bias[e];
-            st_co(logits + (size_t)tid * E + e, ((uint64_t)tag << 32) | __float_as_uint(s));
-        }
-        __syncthreads();
     }
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        if (t < T) {
+            const float s = wave_sum(acc_t[t]);
+            if (lane == 0) red[wv * kTMax + t] = s;
+        }
+    }
+    __syncthreads();
+    if (tid < T) {
+        float s = 0.0f;
+        for (int v = 0; v < kWaves; ++v) s += red[v * kTMax + tid];
+        if (p.bias) s += p.bias[e];
+        st_co(logits + (size_t)tid * E + e, ((uint64_t)tag << 32) | __float_as_uint(s));
+    }
+    __syncthreads();
 }
 
 }  // namespace monomoe

@@ -34,11 +34,15 @@ constexpr int kQMax = 640;                    // segments per forward
 //    data (logits, SiLU activations, output contributions) is written as 8-byte words
 //    {value, tag}, and a reader knows a word is from this launch when its tag matches.
 //    Nothing is reset between launches.
+//  * ids: the multi-tile kernel's exchange of selected experts, {expert id, tag} words
+//    [T*k] (8-byte aligned).
 enum : int {
     kCtlStatus = 0,
     kCtlEpoch = 64,                       // [kGridMax]
+    kCtlIds = kCtlEpoch + kGridMax,       // [2 * kPMax]
 };
-constexpr int ctl_words() { return kCtlEpoch + kGridMax; }
+static_assert(kCtlIds % 2 == 0, "8-byte words");
+constexpr int ctl_words() { return kCtlIds + 2 * kPMax; }
 
 enum : uint32_t { kDevOk = 0, kDevTimeout = 1, kDevBadIds = 2, kDevOverflow = 3 };
 
