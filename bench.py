@@ -65,8 +65,9 @@ def measured_traffic(workload):
             rec = json.load(fh)
     except OSError:
         return None
-    from paper_2609_04244_amd.profile_layer import kernel_source_hash
-    if rec.get("workload") != workload or rec.get("kernel_source_sha256") != kernel_source_hash():
+    from paper_2609_04244_amd.profile_layer import kernel_kind, kernel_source_hash
+    if (rec.get("workload") != workload or
+            rec.get("kernel_source_sha256") != kernel_source_hash(kernel_kind(rec.get("kernel", "")))):
         return None
     per = rec["per_T"]
     if any(str(T) not in per or "fetch_bytes" not in per[str(T)] for T in TS):

@@ -111,14 +111,23 @@ def run(args):
         print("reference copy and read kernels: %d MiB each, 3 launches" % args.copy_mib, flush=True)
 
 
-KERNEL_SOURCES = ("csrc/monomoe_kernel.hip", "csrc/monomoe_internal.h")
+# sources of each kernel (counters and traces are only valid for this code)
+KERNEL_SOURCES = {
+    "single": ("csrc/monomoe_kernel.hip", "csrc/monomoe_device.h", "csrc/monomoe_internal.h"),
+    "multi": ("csrc/monomoe_kernel_mt.hip", "csrc/monomoe_device.h", "csrc/monomoe_internal.h"),
+}
 
 
-def kernel_source_hash():
-    """sha256 over the fused kernel's sources (counters are only valid for this code)."""
+def kernel_kind(kernel_name):
+    """'multi' for the multi-tile kernel's symbol, else 'single'."""
+    return "multi" if "monomoe_fused_mt" in kernel_name else "single"
+
+
+def kernel_source_hash(kind="single"):
+    """sha256 over one kernel's sources."""
     h = hashlib.sha256()
     here = os.path.dirname(os.path.abspath(__file__))
-    for f in KERNEL_SOURCES:
+    for f in KERNEL_SOURCES[kind]:
         with open(os.path.join(here, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
@@ -172,7 +181,7 @@ def summarize(args):
     read_us = min(dur(r) for r in reads) if reads else None
     rec = {
         "kernel": kname, "workload": args.workload, "token_counts": Ts, "launches_per_T": n,
-        "kernel_source_sha256": kernel_source_hash(), "per_T": {},
+        "kernel_source_sha256": kernel_source_hash(kernel_kind(kname)), "per_T": {},
         "copy_kernel": {"bytes_each_way": nbytes, "us_min": copy_us,
                         "GBps_read_plus_write": (2 * nbytes / copy_us / 1e3) if copy_us else None},
         "read_kernel": {"bytes": nbytes, "us_min": read_us,
@@ -273,7 +282,7 @@ def bench_trace(args):
     stats = [f for f in _rows(args.trace) if f.endswith("kernel_stats.csv")]
     lines = ["# bench.py under rocprofv3 --kernel-trace --stats", "",
              "Command (from the repository root; OUT is a scratch directory):", "", "```", args.command.strip(), "```", "",
-             "Kernel source sha256: `%s`" % kernel_source_hash(), "",
+             "Kernel source sha256: `%s`" % kernel_source_hash(kernel_kind(tr[-1]["Kernel_Name"])), "",
              "Fused-kernel launches in the trace: %d (selection pass, warm-up and timed); the last %d are the "
              "timed ones." % (len(tr), len(timed)), "",
              "| source | mean launch us |", "|---|---|",
