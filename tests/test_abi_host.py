@@ -76,3 +76,36 @@ def test_null_arguments():
     assert L.monomoe_plan_reset(None) == mm.MONOMOE_ERR_INVALID
     assert L.monomoe_plan_info(None, None) == mm.MONOMOE_ERR_INVALID
     L.monomoe_plan_destroy(None)
+
+
+def test_binding_structs_match_the_header_layout(tmp_path):
+    # offsetof/sizeof of every field of the header's structs, from a C program compiled
+    # against include/monomoe.h, against the ctypes layouts the binding passes
+    if not os.path.isfile("/opt/rocm/include/hip/hip_runtime_api.h"):
+        pytest.skip("HIP headers not installed")
+    structs = [("monomoe_shape_t", mm.Shape), ("monomoe_debug_t", mm.Debug), ("monomoe_plan_info_t", mm.PlanInfo),
+               ("monomoe_schedule_t", mm.Schedule)]
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "monomoe.h"', "int main(void) {"]
+    for cname, py in structs:
+        lines.append('printf("%s %%zu\\n", sizeof(%s));' % (cname, cname))
+        for f, _ in py._fields_:
+            cf = "as" if f == "as_" else f
+            lines.append('printf("%s.%s %%zu %%zu\\n", offsetof(%s, %s), sizeof(((%s*)0)->%s));'
+                         % (cname, f, cname, cf, cname, cf))
+    lines += ["return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    import subprocess
+    cc = subprocess.run(["gcc", "-std=c99", "-D__HIP_PLATFORM_AMD__", "-I", os.path.dirname(HEADER),
+                         "-I", "/opt/rocm/include", "-o", str(exe), str(src)], capture_output=True, text=True)
+    assert cc.returncode == 0, cc.stderr
+    got = {}
+    for line in subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.splitlines():
+        key, *vals = line.split()
+        got[key] = tuple(int(v) for v in vals)
+    for cname, py in structs:
+        assert got[cname] == (ctypes.sizeof(py),), cname
+        for f, _ in py._fields_:
+            desc = getattr(py, f)
+            assert got["%s.%s" % (cname, f)] == (desc.offset, desc.size), (cname, f)
