@@ -218,6 +218,19 @@ def summarize(args):
                 rec["per_T"].setdefault(str(T), {}).update(
                     {"mfma_busy_cycles": b, "gui_active_cycles": g,
                      "mfma_busy_frac": b / (g / args.xcds * args.cus) if g > 0 else None})
+    extra = []   # counter names of the --pmc runs, in order
+    for d in args.pmc:
+        with open(_find(d, "counter_collection.csv")) as fh:
+            names = sorted({r["Counter_Name"] for r in csv.DictReader(fh)})
+        for name in names:
+            tab = _counter_by_dispatch(d, name)
+            f_ids = [i for i in sorted(tab) if "monomoe_fused" in tab[i][0]]
+            if len(f_ids) != n * len(Ts):
+                raise SystemExit("%s: expected %d fused dispatches, found %d" % (name, n * len(Ts), len(f_ids)))
+            extra.append(name)
+            for i, T in enumerate(Ts):
+                v = [tab[k][1] for k in f_ids[i * n:(i + 1) * n]]
+                rec["per_T"].setdefault(str(T), {}).setdefault("counters", {})[name] = sum(v) / n
     for T in Ts:
         rec["per_T"].setdefault(str(T), {}).update(per_T[T])
     stats = [f for f in _rows(args.trace) if f.endswith("kernel_stats.csv")]
@@ -260,6 +273,13 @@ def summarize(args):
         lines.append("MFMA busy per CU (SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / %d XCDs x %d CUs)): %s." % (
             args.xcds, args.cus, ", ".join("T=%d %.1f%%" % (T, 100 * rec["per_T"][str(T)]["mfma_busy_frac"]) for T in Ts
                                 if rec["per_T"][str(T)].get("mfma_busy_frac") is not None)))
+    if extra:
+        lines += ["", "Further counters, mean per launch (rocprofv3 sums them over the device):", "",
+                  "| counter | " + " | ".join("T=%d" % T for T in Ts) + " |",
+                  "|---|" + "---|" * len(Ts)]
+        for name in extra:
+            lines.append("| %s | " % name + " | ".join("%.4g" % rec["per_T"][str(T)]["counters"][name] for T in Ts)
+                         + " |")
     if rec.get("kernel_stats"):
         lines += ["", "rocprofv3 --stats (all launches of the run):", "",
                   "| kernel | calls | average ns | min ns | max ns |", "|---|---|---|---|---|"]
@@ -330,6 +350,9 @@ def main():
     m.add_argument("--fetch", help="output directory of the --pmc FETCH_SIZE run")
     m.add_argument("--write", help="output directory of the --pmc WRITE_SIZE run")
     m.add_argument("--mfma", help="output directory of a --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE run")
+    m.add_argument("--pmc", action="append", default=[],
+                   help="output directory of any further --pmc run: every counter it holds is reported "
+                        "as a mean per fused launch (repeatable)")
     m.add_argument("--cus", type=int, default=256)
     m.add_argument("--xcds", type=int, default=8)
     m.add_argument("--T", default="1,2,4,8")
