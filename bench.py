@@ -14,6 +14,12 @@ Printed (one JSON line): value = algorithmic bytes of the step / summed launch t
 per-T latency (mean and p50, microseconds), achieved GB/s and fraction of the 8 TB/s peak;
 a roofline object for the kernel; and the CPU oracle timed on a bounded sample.
 
+Other layers and token counts (up to 64, where the multi-tile kernel runs) are a flag away:
+`--workload coarse --tokens 16,32,64`; the workload's routing policy (softmax, or sigmoid
+with a selection bias) is applied to every plan.  The roofline's measured traffic is the
+committed FETCH_SIZE/WRITE_SIZE record of each T's kernel on that workload, when there is
+one and its kernel sources are unchanged.
+
 Algorithmic bytes of one launch: every selected expert's weights read once,
 U * 3*H*I fp8 bytes plus their fp32 block scales U * 3*H*I/4096, plus the router
 weight E*H*2, the input T*H*2 and the output T*H*2 bytes.
@@ -29,10 +35,10 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
 TS = (1, 2, 4, 8)
-# HBM counter record of this workload (rocprofv3 FETCH_SIZE / WRITE_SIZE passes over the
-# C++ profiling driver, calibrated on a plain copy kernel); used only while the kernel
-# sources still hash to the value it was taken on.
-COUNTERS = os.path.join(ROOT, "profiles", "monomoe_fused_small_expert_counters.json")
+# HBM counter records (rocprofv3 FETCH_SIZE / WRITE_SIZE passes over the C++ profiling
+# driver, calibrated on a plain copy kernel), one per kernel and workload; a record is used
+# only while its kernel's sources still hash to the value it was taken on.
+PROFILES = os.path.join(ROOT, "profiles")
 
 
 def parse():
@@ -41,6 +47,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="small_expert")
+    ap.add_argument("--tokens", default="1,2,4,8",
+                    help="decode token counts of one step (up to 64; the metric is quoted on 1,2,4,8)")
     ap.add_argument("--layers", type=int, default=16)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -56,23 +64,26 @@ def algorithmic_bytes(U, T, H, E, I):
     return weights + scales + E * H * 2 + 2 * T * H * 2
 
 
-def measured_traffic(workload):
+def measured_traffic(workload, kinds):
     """HBM bytes per launch (read + write, mean over the step's token counts) from the
-    committed counter record, or None when there is none for this workload or the kernel
-    sources changed since it was taken."""
-    try:
-        with open(COUNTERS) as fh:
-            rec = json.load(fh)
-    except OSError:
-        return None
+    committed counter records, or None unless every token count T has a record of this
+    workload, taken on the kernel that runs at T (kinds[T], "single" or "multi") whose
+    sources have not changed since."""
+    import glob
     from paper_2609_04244_amd.profile_layer import kernel_kind, kernel_source_hash
-    if (rec.get("workload") != workload or
-            rec.get("kernel_source_sha256") != kernel_source_hash(kernel_kind(rec.get("kernel", "")))):
+    per = {}
+    for path in sorted(glob.glob(os.path.join(PROFILES, "*_counters.json"))):
+        with open(path) as fh:
+            rec = json.load(fh)
+        kind = kernel_kind(rec.get("kernel", ""))
+        if rec.get("workload") != workload or rec.get("kernel_source_sha256") != kernel_source_hash(kind):
+            continue
+        for T, v in rec.get("per_T", {}).items():
+            if "fetch_bytes" in v and kinds.get(int(T)) == kind:
+                per.setdefault(int(T), v["fetch_bytes"] + v["write_bytes"])
+    if any(T not in per for T in TS):
         return None
-    per = rec["per_T"]
-    if any(str(T) not in per or "fetch_bytes" not in per[str(T)] for T in TS):
-        return None
-    return sum(per[str(T)]["fetch_bytes"] + per[str(T)]["write_bytes"] for T in TS) / len(TS)
+    return sum(per[T] for T in TS) / len(TS)
 
 
 def main():
@@ -87,6 +98,8 @@ def main():
     from paper_2609_04244_amd import monomoe as mm
     from paper_2609_04244_amd import workloads as wl
 
+    global TS
+    TS = tuple(int(t) for t in args.tokens.split(","))
     cfg = wl.config(args.workload)
     H, E, I, k, renorm = cfg["H"], cfg["E"], cfg["I"], cfg["k"], cfg["renorm"]
     dev = torch.device("cuda:0")
@@ -97,11 +110,16 @@ def main():
     outs = {T: torch.empty((T, H), dtype=torch.bfloat16, device=dev) for T in TS}
     xs = {(l, T): layers[l]["x"][:T].contiguous() for l in range(args.layers) for T in TS}
 
+    def route(p, L):   # the layer's routing inputs (logit bias; sigmoid selection bias)
+        if L["bias"] is not None:
+            p.set_router_bias(L["bias"])
+        if L["policy"] == "sigmoid_bias":
+            p.set_routing(mm.ROUTING_SIGMOID_BIAS, L["sel_bias"], L["route_scale"])
+
     def launch(l, T, timer):
         L = layers[l]
         p = plans[T]
-        if L["bias"] is not None:
-            p.set_router_bias(L["bias"])
+        route(p, L)
         p.forward_timed(xs[(l, T)], L["router_w"], L["w13"], L["w13_scale"], L["w2"], L["w2_scale"], outs[T], timer)
 
     # unique experts of every (layer, T), from the operator's own selection (untimed)
@@ -109,8 +127,7 @@ def main():
     for l in range(args.layers):
         for T in TS:
             L = layers[l]
-            if L["bias"] is not None:
-                plans[T].set_router_bias(L["bias"])
+            route(plans[T], L)
             _, d = plans[T].forward_debug(xs[(l, T)], L["router_w"], L["w13"], L["w13_scale"], L["w2"],
                                           L["w2_scale"])
             torch.cuda.synchronize()
@@ -178,18 +195,23 @@ def main():
         wbytes_tot += float(np.sum(wb))
     value = tot_bytes / (tot_ms * 1e-3) / 1e9
     ms_per_step = w_start.elapsed_time(w_end) / args.steps
-    traffic = measured_traffic(args.workload)
+    kinds = {T: "multi" if plans[T].info()["multi_tile"] else "single" for T in TS}
+    traffic = measured_traffic(args.workload, kinds)
 
     res = {
-        "metric": "routed-MoE op latency us + achieved HBM GB/s (% of peak) at T=1,2,4,8 tokens",
+        "metric": "routed-MoE op latency us + achieved HBM GB/s (% of peak) at T=" + ",".join(map(str, TS)) + " tokens",
         "value": round(float(value), 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(float(ms_per_step), 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "fp8_e4m3 (fp32 accumulate)", "data": "synthetic",
         "config": {
-            "workload": "%s: H=%d E=%d I=%d top-%d %s softmax, block-FP8 128x128 weights, T in %s, "
-                        "%d rotated layers" % (args.workload, H, E, I, k, "renormalised" if renorm else "plain",
+            "workload": "%s: H=%d E=%d I=%d top-%d %s, block-FP8 128x128 weights, T in %s, "
+                        "%d rotated layers" % (args.workload, H, E, I, k,
+                                               "sigmoid routing with selection bias"
+                                               if cfg.get("policy") == "sigmoid_bias" else
+                                               ("renormalised" if renorm else "plain") + " softmax",
                                                list(TS), args.layers),
-            "launches_per_step": len(TS), "grid": plans[1].info()["grid"], "block": plans[1].info()["block"],
+            "launches_per_step": len(TS), "grid": plans[TS[0]].info()["grid"],
+            "block": plans[TS[0]].info()["block"],
         },
         "per_T": per_T,
         "roofline": {
@@ -198,7 +220,8 @@ def main():
             "traffic": None if traffic is None else round(float(traffic)),
             "traffic_unit": "HBM bytes per launch (read + write, mean over T)",
             "algorithmic_bytes_per_launch": round(float(tot_bytes / (args.steps * len(TS)))),
-            "kernel": "monomoe_fused<%d,%d>" % (H, I),
+            "kernel": ", ".join(sorted({"monomoe_fused%s<%d,%d>" % ("_mt" if plans[T].info()["multi_tile"] else "", H, I)
+                                        for T in TS})),
             "launch_us_mean": round(float(tot_ms / (args.steps * len(TS)) * 1e3), 2),
         },
         "wall_s_timed": round(wall, 3),
@@ -214,19 +237,26 @@ def main():
 
 def cpu_baseline(args, layers, U, plans, outs, xs, cfg, wbytes_step, bytes_step):
     """The fp64 oracle on the host cores, on a bounded sample of the same workload: the
-    step's four forwards (T = 1, 2, 4, 8) on layer 0, repeated while under the time budget.
+    step's forwards (one per token count) on layer 0, repeated while under the time budget.
     Also checks the operator's outputs on those forwards against the oracle."""
     import numpy as np
     import torch
     from oracle import oracle
+    from paper_2609_04244_amd import monomoe as mm
     from paper_2609_04244_amd import workloads as wl
 
     H, E, I, k, renorm = cfg["H"], cfg["E"], cfg["I"], cfg["k"], cfg["renorm"]
     L = layers[0]
     rw = wl.bf16_bits(L["router_w"])
     bias = None if L["bias"] is None else L["bias"].cpu().numpy()
+    sigmoid = L["policy"] == "sigmoid_bias"
+    sel_bias = None if not sigmoid or L["sel_bias"] is None else L["sel_bias"].cpu().numpy()
+    route = dict(policy=oracle.SIGMOID_BIAS, sel_bias=sel_bias, scale=L["route_scale"]) if sigmoid else {}
     logits = oracle.router_logits(wl.bf16_bits(L["x"]), rw, bias)
-    ids, _ = oracle.select(logits, k, renorm)
+    if sigmoid:
+        ids, _ = oracle.select_sigmoid(logits, k, sel_bias, L["route_scale"])
+    else:
+        ids, _ = oracle.select(logits, k, renorm)
     ex = sorted(set(ids.reshape(-1).tolist()))
     idx = torch.tensor(ex, device=L["w13"].device)
     host = [t.index_select(0, idx).cpu().numpy() for t in (L["w13"], L["w13_scale"], L["w2"], L["w2_scale"])]
@@ -237,11 +267,13 @@ def cpu_baseline(args, layers, U, plans, outs, xs, cfg, wbytes_step, bytes_step)
     reps = 0
     while True:
         for T in TS:
-            ref = oracle.forward(wl.bf16_bits(xs[(0, T)]), rw, *tabs, k, renorm, bias=bias)
+            ref = oracle.forward(wl.bf16_bits(xs[(0, T)]), rw, *tabs, k, renorm, bias=bias, **route)
             if reps == 0:
                 p = plans[T]
                 if L["bias"] is not None:
                     p.set_router_bias(L["bias"])
+                if sigmoid:
+                    p.set_routing(mm.ROUTING_SIGMOID_BIAS, L["sel_bias"], L["route_scale"])
                 out = p.forward(xs[(0, T)], L["router_w"], L["w13"], L["w13_scale"], L["w2"], L["w2_scale"])
                 torch.cuda.synchronize()
                 got = out.float().cpu().numpy().astype(np.float64)
@@ -257,8 +289,8 @@ def cpu_baseline(args, layers, U, plans, outs, xs, cfg, wbytes_step, bytes_step)
     by0 = sum(algorithmic_bytes(U[(0, T)], T, H, E, I) for T in TS)
     return {
         "value": round(by0 / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-        "sample": "the step's 4 forwards (T=1,2,4,8) on layer 0, %d repetition(s), %.2f s each; "
-                  "%d selected experts in total" % (reps, dt, u0),
+        "sample": "the step's %d forwards (T=%s) on layer 0, %d repetition(s), %.2f s each; "
+                  "%d selected experts in total" % (len(TS), ",".join(map(str, TS)), reps, dt, u0),
         "ms_per_step": round(dt * 1e3, 1),
         "gpu_vs_oracle_max_err_over_rms": round(worst, 5), "gpu_vs_oracle_mean_rel_err": round(mre_worst, 6),
     }
