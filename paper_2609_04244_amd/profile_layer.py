@@ -315,9 +315,13 @@ def bench_trace(args):
                      u["roofline"]["launch_us_mean"])
     lines += ["", "(Under the tracer the event stamps include its own per-dispatch work; without it the "
               "dispatch-stamped events and the kernel trace agree.)", ""]
-    lines.append("bench.py line: value %.1f GB/s (%.1f%% of 8 TB/s); per T: %s." % (
-        b["value"], 100 * b["roofline"]["frac"],
-        ", ".join("T=%s %.2f us" % (k, v["us_mean"]) for k, v in b["per_T"].items())))
+    def line(r):
+        return "value %.1f GB/s (%.1f%% of 8 TB/s); per T: %s" % (
+            r["value"], 100 * r["roofline"]["frac"],
+            ", ".join("T=%s %.2f us" % (k, v["us_mean"]) for k, v in r["per_T"].items()))
+    lines.append("bench.py line under the tracer: %s." % line(b))
+    if args.untraced_json:
+        lines += ["", "bench.py line without the tracer: %s." % line(u)]
     if stats:
         with open(stats[0]) as fh:
             rows = [r for r in csv.DictReader(fh)]
