@@ -10,10 +10,14 @@
  * kernel with four logical stages linked by readiness flags).
  *
  * The operator interface follows the paper's generic form (Sec. 3.4): the model shape
- * is fixed per plan, the token count is part of the plan's shape, top-k and the
- * routing policy (softmax, with or without renormalisation, optional per-expert logit
- * bias) are plan parameters; X is the input tile, R the routing inputs (router weight
- * and optional bias), W_gu/W_down the expert weights and S their block scales.
+ * is fixed per plan together with a token bound T (the paper's B_max); the token count of
+ * a call is a runtime argument up to that bound (monomoe_forward_tokens; monomoe_forward
+ * runs exactly T).  Top-k and the renormalisation flag are fixed per plan (the paper makes
+ * k a runtime argument: a deviation, since k sizes the routing tables and the workspace);
+ * the routing policy and its inputs (softmax or sigmoid routing, optional per-expert
+ * logit bias, selection bias, scaling factor) are set on a plan between calls.  X is the
+ * input tile, R the routing inputs (router weight and biases), W_gu/W_down the expert
+ * weights and S their block scales.
  *
  * Conventions for every entry point:
  *  - All tensor pointers are DEVICE pointers owned by the caller.  The library never
@@ -21,11 +25,13 @@
  *  - Tensor pointers must be 16-byte aligned and tensors densely packed, row-major.
  *  - Entry points return MONOMOE_OK (0) or a negative monomoe_status_t.  An argument
  *    error enqueues nothing.
- *  - monomoe_forward() and monomoe_forward_debug() never synchronise, never allocate,
- *    and enqueue one kernel on the given stream (consecutive kernels only for a schedule
- *    that forces the single-tile kernel on more tokens than its tile, see
- *    monomoe_plan_set_schedule), so they can be captured into a HIP graph.  A plan owns device workspace: one plan must not be used by two launches
- *    that can overlap (use one plan per stream).
+ *  - monomoe_forward(), monomoe_forward_tokens() and monomoe_forward_debug() never
+ *    synchronise, never allocate, and enqueue one kernel on the given stream (consecutive
+ *    kernels only for a schedule that forces the single-tile kernel on more tokens than
+ *    its tile, see monomoe_plan_set_schedule), so they can be captured into a HIP graph
+ *    and replayed (the kernel's arguments are fixed at capture; the inputs are read from
+ *    the captured pointers at every replay).  A plan owns device workspace: one plan must
+ *    not be used by two launches that can overlap (use one plan per stream).
  *  - The kernel reports failures it detects on the device (a bounded wait that expired)
  *    through a status word read with monomoe_plan_status().
  */
@@ -75,9 +81,11 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
  * the plan is still pending.  NULL is ignored. */
 void monomoe_plan_destroy(monomoe_plan_t plan);
 
-/* Optional routing input: a per-expert fp32 bias [E] (device pointer, or NULL to remove)
- * added to the router logits before softmax and selection, so it changes both the
- * selected experts and their weights.  The pointer is read by every later forward. */
+/* Optional routing input (paper Sec. 3.4: R, the operator's routing inputs, beside the
+ * router weight): a per-expert fp32 bias [E] (device pointer, or NULL to remove) added to
+ * the router logits before softmax and selection, so it changes both the selected experts
+ * and their weights.  The pointer is read by every later forward.  Returns
+ * MONOMOE_ERR_INVALID for a NULL plan or a pointer that is not 16-byte aligned. */
 int monomoe_plan_set_router_bias(monomoe_plan_t plan, const float* bias);
 
 /* Routing policy (paper Sec. 4.1: softmax routing for the Qwen models; sigmoid routing
@@ -109,6 +117,20 @@ int monomoe_forward(monomoe_plan_t plan, const void* x, const void* router_w,
                     const void* w13, const float* w13_scale,
                     const void* w2, const float* w2_scale,
                     void* out, hipStream_t stream);
+
+/* The operator on T tokens, for any T in [0, the plan's T], without re-planning (paper
+ * Sec. 3.4: the decode batch size B <= B_max is a runtime argument of the operator; here the
+ * plan's T is B_max).  x is bf16 [T,H] and out bf16 [T,H]; every other argument and the
+ * asynchrony are as for monomoe_forward, and T == 0 enqueues nothing.  The kernel is chosen per
+ * call: when the plan's T needs the multi-tile kernel, a call with at most one single-tile
+ * kernel tile of tokens takes the single-tile kernel instead (unless the plan's schedule
+ * forces a kernel, or the layer's down projection is sliced, see monomoe_plan_info).  The
+ * plan's workspace, sized for its T, serves every smaller T.  Returns MONOMOE_ERR_INVALID
+ * (nothing enqueued) for T outside [0, the plan's T]. */
+int monomoe_forward_tokens(monomoe_plan_t plan, int32_t T, const void* x, const void* router_w,
+                           const void* w13, const float* w13_scale,
+                           const void* w2, const float* w2_scale,
+                           void* out, hipStream_t stream);
 
 /* Test hooks.  Every pointer may be NULL.  Pair index p = t*topk + j.
  *   topk_ids  int32 [T,topk]      selected experts, in selection order (written)

@@ -45,6 +45,9 @@ struct monomoe_plan_s {
     int tchunk;   // tokens per pass (T larger than one LDS-resident tile runs in passes)
     int mt;       // multi-tile kernel
     int mt_rows, mt_pool, mt_tiles;
+    KernelConfig cfg;           // the configuration above, as chosen for T
+    KernelConfig small;         // single-tile configuration for forwards of at most small_T
+    int small_T;                //   tokens when cfg is the multi-tile kernel (0: none)
     const float* bias;
     const float* sel_bias;
     int policy;
@@ -67,6 +70,15 @@ constexpr uint64_t kDefaultSpinTicks = 200000000ull;   // 2 s of the 100 MHz rea
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// The dynamic-LDS limit of a kernel symbol is process-wide state shared by every plan that
+// launches it, so it is raised to the most any plan can request (all of the workgroup's LDS
+// beyond the kernel's static share) and never lowered: a plan created later with a smaller
+// footprint must not invalidate the launches of an earlier, larger one.
+hipError_t allow_full_lds(const void* fn, int lds_total, const hipFuncAttributes* attr) {
+    return hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               lds_total - (int)attr->sharedSizeBytes);
+}
 
 // Single-tile kernel at ring depth `ring`: the largest token tile (<= kTMax, <= T) whose
 // LDS footprint fits, the requantised activation double-buffered when it fits, then as
@@ -96,8 +108,7 @@ int config_single(const monomoe_plan_s* pl, int ring, KernelConfig* c) {
     for (const KernelVariant& v : pl->kern->v) {
         hipFuncAttributes va;
         int o = 0;
-        if (hipFuncGetAttributes(&va, v.fn) != hipSuccess ||
-            hipFuncSetAttribute(v.fn, hipFuncAttributeMaxDynamicSharedMemorySize, k.lds_dyn) != hipSuccess ||
+        if (hipFuncGetAttributes(&va, v.fn) != hipSuccess || allow_full_lds(v.fn, pl->lds_total, &va) != hipSuccess ||
             hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, v.fn, kThreads, (size_t)k.lds_dyn) != hipSuccess)
             return MONOMOE_ERR_HIP;
         if ((int)va.sharedSizeBytes + k.lds_dyn > pl->lds_total) return MONOMOE_ERR_UNSUPPORTED;
@@ -140,7 +151,7 @@ int config_multi(const monomoe_plan_s* pl, int group_cap, KernelConfig* c) {
     k.tchunk = T;
     k.lds_dyn = mt_region_bytes(s.H, s.I, k.pool, R) + mt_partials_bytes(k.nslots, k.tiles);
     int o = 0;
-    if (hipFuncSetAttribute(k.var->fn, hipFuncAttributeMaxDynamicSharedMemorySize, k.lds_dyn) != hipSuccess ||
+    if (allow_full_lds(k.var->fn, pl->lds_total, &attr) != hipSuccess ||
         hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, k.var->fn, kThreads, (size_t)k.lds_dyn) != hipSuccess)
         return MONOMOE_ERR_HIP;
     if (o < 1) return MONOMOE_ERR_OCCUPANCY;
@@ -156,7 +167,12 @@ int config_multi(const monomoe_plan_s* pl, int group_cap, KernelConfig* c) {
 // LDS before its first down task, which the sliced kernel splits over the slices
 // (measured on the 4096x14336 layer: 272 vs 313 us at T = 8, 321 vs 646 us at T = 16; at
 // T = 1 the two kernels are within 2% of each other).
-int configure(const monomoe_plan_s* pl, int kernel, int ring, int group_cap, KernelConfig* c) {
+// When the automatic choice is the multi-tile kernel for the plan's T, *small receives the
+// single-tile configuration and *small_T the token counts up to which a forward with fewer
+// tokens (monomoe_forward_tokens) takes it instead (0: every T takes *c).
+int configure(const monomoe_plan_s* pl, int kernel, int ring, int group_cap, KernelConfig* c,
+              KernelConfig* small, int* small_T) {
+    *small_T = 0;
     if (kernel == MONOMOE_KERNEL_MULTI) {
         if (ring != 0 && ring != pl->mtv->ring) return MONOMOE_ERR_INVALID;
         return config_multi(pl, group_cap, c);
@@ -168,11 +184,20 @@ int configure(const monomoe_plan_s* pl, int kernel, int ring, int group_cap, Ker
     if (rc != MONOMOE_OK || kernel == MONOMOE_KERNEL_SINGLE || (pl->shape.T <= c->tchunk && !sliced)) return rc;
     if (ring != 0 && ring != pl->mtv->ring) return MONOMOE_OK;   // that depth exists in the single-tile kernel only
     KernelConfig m;
-    if (config_multi(pl, group_cap, &m) == MONOMOE_OK) *c = m;
+    if (config_multi(pl, group_cap, &m) == MONOMOE_OK) {
+        if (!sliced) {
+            *small = *c;
+            *small_T = c->tchunk;
+        }
+        *c = m;
+    }
     return MONOMOE_OK;
 }
 
-void apply_config(monomoe_plan_s* pl, const KernelConfig& c) {
+void apply_config(monomoe_plan_s* pl, const KernelConfig& c, const KernelConfig& small, int small_T) {
+    pl->cfg = c;
+    pl->small = small;
+    pl->small_T = small_T;
     pl->var = c.var;
     pl->mt = c.mt;
     pl->occupancy = c.occupancy;
@@ -192,12 +217,15 @@ int zero_workspace(monomoe_plan_s* pl) {
     return MONOMOE_OK;
 }
 
-int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void* w13, const float* w13_scale,
+// One forward of T tokens (0 <= T <= the plan's T) with the plan's configuration for T.
+int launch(monomoe_plan_t plan, int T, const void* x, const void* router_w, const void* w13, const float* w13_scale,
            const void* w2, const float* w2_scale, void* out, const monomoe_debug_t* dbg, hipStream_t stream,
            hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr) {
     if (!plan) return MONOMOE_ERR_INVALID;
     const monomoe_shape_t& s = plan->shape;
-    if (s.T == 0) return MONOMOE_OK;
+    if (T < 0 || T > s.T) return MONOMOE_ERR_INVALID;
+    if (T == 0) return MONOMOE_OK;
+    const KernelConfig& cf = (T <= plan->small_T) ? plan->small : plan->cfg;
     if (!x || !router_w || !w13 || !w13_scale || !w2 || !w2_scale || !out) return MONOMOE_ERR_INVALID;
     if (!aligned16(x) || !aligned16(router_w) || !aligned16(w13) || !aligned16(w2) || !aligned16(out) ||
         !aligned16(w13_scale) || !aligned16(w2_scale))
@@ -245,20 +273,20 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
     p.E = s.E;
     p.k = plan->topk;
     p.renorm = plan->renorm;
-    p.naq = plan->naq;
-    p.nslots = plan->nslots;
-    p.mt_rows = (uint8_t)plan->mt_rows;
-    p.mt_tiles = (uint8_t)plan->mt_tiles;
-    p.mt_pool = (uint16_t)plan->mt_pool;
+    p.naq = cf.naq;
+    p.nslots = cf.nslots;
+    p.mt_rows = (uint8_t)cf.rows;
+    p.mt_tiles = (uint8_t)cf.tiles;
+    p.mt_pool = (uint16_t)cf.pool;
 
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess || cur != plan->device) return MONOMOE_ERR_INVALID;
     // one launch per pass of at most tchunk tokens (one pass when T fits one tile); each
     // pass sees its rows of every token-indexed buffer
-    const int K = plan->topk, H = s.H, I = s.I, tc = plan->mt ? s.T : plan->tchunk;
-    for (int t0 = 0; t0 < s.T; t0 += tc) {
+    const int K = plan->topk, H = s.H, I = s.I, tc = cf.mt ? T : cf.tchunk;
+    for (int t0 = 0; t0 < T; t0 += tc) {
         KParams q = p;
-        q.T = std::min(tc, s.T - t0);
+        q.T = std::min(tc, T - t0);
         q.x = p.x + (size_t)t0 * H;
         q.out = p.out + (size_t)t0 * H;
         if (p.d_ids) q.d_ids = p.d_ids + (size_t)t0 * K;
@@ -271,16 +299,16 @@ int launch(monomoe_plan_t plan, const void* x, const void* router_w, const void*
         if (p.d_out) q.d_out = p.d_out + (size_t)t0 * H;
         if (p.inj_ids) q.inj_ids = p.inj_ids + (size_t)t0 * K;
         if (p.inj_w) q.inj_w = p.inj_w + (size_t)t0 * K;
-        const bool first = t0 == 0, last = t0 + tc >= s.T;
+        const bool first = t0 == 0, last = t0 + tc >= T;
         if (ev_start || ev_stop) {
             // the dispatch itself records the events (the first pass's begin, the last
             // pass's end), not the stream
             void* args[] = {&q};
-            if (hipExtLaunchKernel(plan->var->fn, dim3(plan->grid), dim3(kThreads), args, (size_t)plan->lds_dyn,
+            if (hipExtLaunchKernel(cf.var->fn, dim3(plan->grid), dim3(kThreads), args, (size_t)cf.lds_dyn,
                                    stream, first ? ev_start : nullptr, last ? ev_stop : nullptr, 0) != hipSuccess)
                 return MONOMOE_ERR_HIP;
         } else {
-            plan->var->launch(q, plan->grid, (size_t)plan->lds_dyn, stream);
+            cf.var->launch(q, plan->grid, (size_t)cf.lds_dyn, stream);
         }
         if (hipGetLastError() != hipSuccess) return MONOMOE_ERR_HIP;
     }
@@ -336,13 +364,14 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
     pl->device = dev;
     pl->num_cus = prop.multiProcessorCount;
     pl->lds_total = (int)prop.sharedMemPerBlock;
-    KernelConfig cfg;
-    const int cr = configure(pl, MONOMOE_KERNEL_AUTO, 0, 0, &cfg);
+    KernelConfig cfg{}, small{};
+    int small_T = 0;
+    const int cr = configure(pl, MONOMOE_KERNEL_AUTO, 0, 0, &cfg, &small, &small_T);
     if (cr != MONOMOE_OK) {
         delete pl;
         return cr;
     }
-    apply_config(pl, cfg);
+    apply_config(pl, cfg, small, small_T);
     {
         hipFuncAttributes attr;
         if (hipFuncGetAttributes(&attr, pl->var->fn) != hipSuccess) {
@@ -428,11 +457,13 @@ int monomoe_plan_set_schedule(monomoe_plan_t plan, const monomoe_schedule_t* sch
     if (sched->ring != 0 && sched->ring != kRings[0] && sched->ring != kRings[1]) return MONOMOE_ERR_INVALID;
     int dev = -1;
     if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return MONOMOE_ERR_INVALID;
-    KernelConfig cfg;
-    const int cr = configure(plan, sched->kernel, sched->ring, sched->group_tokens, &cfg);
+    KernelConfig cfg{}, small{};
+    int small_T = 0;
+    const int cr = configure(plan, sched->kernel, sched->ring, sched->group_tokens, &cfg, &small, &small_T);
     if (cr != MONOMOE_OK) return cr;
     const int grid = sched->grid == 0 ? plan->num_cus : sched->grid;
     if (grid < 1 || grid > plan->num_cus * cfg.occupancy || grid > kGridMax) return MONOMOE_ERR_INVALID;
+    if (small_T > 0 && grid > plan->num_cus * small.occupancy) small_T = 0;
     // the launch epochs are per workgroup: a new grid starts from a clean workspace
     if (grid != plan->grid) {
         if (hipDeviceSynchronize() != hipSuccess) return MONOMOE_ERR_HIP;
@@ -440,26 +471,34 @@ int monomoe_plan_set_schedule(monomoe_plan_t plan, const monomoe_schedule_t* sch
         if (zr != MONOMOE_OK) return zr;
     }
     plan->grid = grid;
-    apply_config(plan, cfg);
+    apply_config(plan, cfg, small, small_T);
     return MONOMOE_OK;
 }
 
 int monomoe_forward(monomoe_plan_t plan, const void* x, const void* router_w, const void* w13,
                     const float* w13_scale, const void* w2, const float* w2_scale, void* out, hipStream_t stream) {
-    return launch(plan, x, router_w, w13, w13_scale, w2, w2_scale, out, nullptr, stream);
+    if (!plan) return MONOMOE_ERR_INVALID;
+    return launch(plan, plan->shape.T, x, router_w, w13, w13_scale, w2, w2_scale, out, nullptr, stream);
+}
+
+int monomoe_forward_tokens(monomoe_plan_t plan, int32_t T, const void* x, const void* router_w, const void* w13,
+                           const float* w13_scale, const void* w2, const float* w2_scale, void* out,
+                           hipStream_t stream) {
+    return launch(plan, T, x, router_w, w13, w13_scale, w2, w2_scale, out, nullptr, stream);
 }
 
 int monomoe_forward_timed(monomoe_plan_t plan, const void* x, const void* router_w, const void* w13,
                           const float* w13_scale, const void* w2, const float* w2_scale, void* out,
                           hipEvent_t start, hipEvent_t stop, hipStream_t stream) {
-    if (!start || !stop) return MONOMOE_ERR_INVALID;
-    return launch(plan, x, router_w, w13, w13_scale, w2, w2_scale, out, nullptr, stream, start, stop);
+    if (!plan || !start || !stop) return MONOMOE_ERR_INVALID;
+    return launch(plan, plan->shape.T, x, router_w, w13, w13_scale, w2, w2_scale, out, nullptr, stream, start, stop);
 }
 
 int monomoe_forward_debug(monomoe_plan_t plan, const void* x, const void* router_w, const void* w13,
                           const float* w13_scale, const void* w2, const float* w2_scale, void* out,
                           const monomoe_debug_t* dbg, hipStream_t stream) {
-    return launch(plan, x, router_w, w13, w13_scale, w2, w2_scale, out, dbg, stream);
+    if (!plan) return MONOMOE_ERR_INVALID;
+    return launch(plan, plan->shape.T, x, router_w, w13, w13_scale, w2, w2_scale, out, dbg, stream);
 }
 
 int monomoe_plan_status(monomoe_plan_t plan) {

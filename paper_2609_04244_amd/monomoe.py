@@ -28,7 +28,7 @@ KERNEL_MULTI = 2
 EXPORTS = (
     "monomoe_plan", "monomoe_plan_destroy", "monomoe_plan_set_router_bias", "monomoe_plan_set_routing",
     "monomoe_plan_set_schedule",
-    "monomoe_forward",
+    "monomoe_forward", "monomoe_forward_tokens",
     "monomoe_forward_debug", "monomoe_forward_timed", "monomoe_plan_status", "monomoe_plan_reset", "monomoe_plan_info",
     "monomoe_supported_shape", "monomoe_status_string", "monomoe_stream_copy", "monomoe_stream_read",
 )
@@ -88,6 +88,8 @@ def lib():
         L.monomoe_plan_set_schedule.restype = ctypes.c_int
         L.monomoe_forward.argtypes = [vp] * 9
         L.monomoe_forward.restype = ctypes.c_int
+        L.monomoe_forward_tokens.argtypes = [vp, ctypes.c_int32] + [vp] * 8
+        L.monomoe_forward_tokens.restype = ctypes.c_int
         L.monomoe_forward_debug.argtypes = [vp] * 8 + [ctypes.POINTER(Debug), vp]
         L.monomoe_forward_debug.restype = ctypes.c_int
         L.monomoe_forward_timed.argtypes = [vp] * 11
@@ -277,6 +279,27 @@ class Plan:
                                    _ptr(w2_scale), _ptr(out), _stream(stream))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_forward")
+        return out
+
+    def forward_tokens(self, T, x, router_w, w13, w13_scale, w2, w2_scale, out=None, stream=None, check=True):
+        """The operator on the first T tokens of the plan's bound (0 <= T <= plan T): x and out
+        are [T,H]; no re-planning.  Returns out."""
+        T = int(T)
+        if out is None:
+            out = torch.empty((T, self.H), dtype=torch.bfloat16, device=x.device)
+        if check:
+            if not 0 <= T <= self.T:
+                raise ValueError("T=%d outside [0, %d]" % (T, self.T))
+            saved = self.T
+            self.T = T
+            try:
+                self._check(x, router_w, w13, w13_scale, w2, w2_scale, out)
+            finally:
+                self.T = saved
+        rc = lib().monomoe_forward_tokens(self._h, T, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale),
+                                          _ptr(w2), _ptr(w2_scale), _ptr(out), _stream(stream))
+        if rc != MONOMOE_OK:
+            raise MonoMoEError(rc, "monomoe_forward_tokens")
         return out
 
     def forward_timed(self, x, router_w, w13, w13_scale, w2, w2_scale, out, timer, stream=None):

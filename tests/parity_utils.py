@@ -8,11 +8,19 @@ run the oracle on the same bytes, and compare under the operator's correctness c
   * requantisation bit-exact when the GPU's own fp32 SiLU(gate)*up is fed to the
     oracle's quantiser;
   * output: max|out - ref| <= 2e-2 * rms(ref) and sum|out - ref| / sum|ref| <= 5e-3, where
-    ref is the oracle's unrounded fp64 result.  The bound is applied to the operator's
-    fp32 result before its final rounding (a test hook), and to the bf16 output with half
-    a bf16 ulp of ref added per element: that rounding is the output format itself, and
-    on its own it can exceed 2e-2 * rms(ref) for a large output element.  The bf16
-    output must be exactly the round-to-nearest-even of the fp32 result.
+    out is the bf16 output and ref the oracle's unrounded fp64 result, exactly as the
+    contract states them.  The same two bounds are also asserted on the operator's fp32
+    result before its final rounding (a test hook), and the bf16 output must be exactly
+    the round-to-nearest-even of that fp32 result.  One exception, decided from the oracle
+    alone: when an output element is so large (about 10 * rms(ref) and beyond, which
+    heavy-tailed Student-t(3) layers produce) that the correctly rounded bf16 of the exact
+    result itself misses the first bound, no bf16 output can meet it; the case is then
+    reported as infeasible in bf16 and each element must instead lie within
+    2e-2 * rms(ref) + half a bf16 ulp of ref (the fp32 result still meets the bound as
+    written).
+  * exact ties: a token whose k-th and (k+1)-th oracle scores are exactly equal has one
+    correct selection under the lower-index rule, so with exact_ties=True its ids are
+    compared bit-exactly as well (the near-tie injection still follows).
 """
 import sys
 
@@ -98,10 +106,20 @@ def _gpu(plan, inp, **kw):
     return h
 
 
-def run_case(inp, tokens=None, plan=None):
+def exact_tie_tokens(logits, k):
+    T, E = logits.shape
+    if k >= E:
+        return np.zeros(T, bool)
+    s = -np.sort(-logits, axis=1)
+    return s[:, k - 1] == s[:, k]
+
+
+def run_case(inp, tokens=None, plan=None, exact_ties=False, min_near_ties=0):
     """Run the GPU operator on `inp` (device tensors from workloads.generate) and compare
     with the oracle on `tokens` (default: all; the oracle's rows are independent per
-    token).  Returns a report dict; raises AssertionError on a contract violation."""
+    token).  exact_ties: also compare the ids of tokens whose boundary scores tie exactly.
+    min_near_ties: the case must contain at least this many near-tie tokens.  Returns a
+    report dict; raises AssertionError on a contract violation."""
     T, H, E, I, k, renorm = inp["T"], inp["H"], inp["E"], inp["I"], inp["k"], inp["renorm"]
     own = plan is None
     if own:
@@ -112,10 +130,13 @@ def run_case(inp, tokens=None, plan=None):
         plan.set_routing(mm.ROUTING_SIGMOID_BIAS, inp["sel_bias"], inp["route_scale"])
     logits, oids, ow = oracle_routing(inp)
     tie = near_tie_tokens(logits, k)
+    assert int(tie.sum()) >= min_near_ties, "expected at least %d near-tie tokens, got %d" % (min_near_ties, tie.sum())
+    exact = exact_tie_tokens(logits, k) if exact_ties else np.zeros(T, bool)
     g = _gpu(plan, inp)
-    # 1. routing: ids bit-exact as sets and weights close, except near-tie tokens
+    # 1. routing: ids bit-exact as sets and weights close, except near-tie tokens (tokens
+    #    with an exact tie have one correct answer and are compared when asked)
     for t in range(T):
-        if tie[t]:
+        if tie[t] and not exact[t]:
             continue
         assert sorted(g["ids"][t].tolist()) == sorted(oids[t].tolist()), \
             "token %d ids %s vs %s" % (t, g["ids"][t], oids[t])
@@ -150,8 +171,8 @@ def run_case(inp, tokens=None, plan=None):
                 q, s = oracle.quantize_group(g["act"][p, gi * 128:(gi + 1) * 128])
                 assert np.array_equal(g["aq"][p, gi * 128:(gi + 1) * 128], q), "aq pair %d group %d" % (p, gi)
                 assert np.float32(g["as"][p, gi]) == np.float32(s), "as pair %d group %d" % (p, gi)
-    # 5. output: the fp32 result strictly, its bf16 rounding exactly, the bf16 output with
-    #    the output format's half ulp
+    # 5. output: the bf16 output under the contract's bounds exactly as written; the same
+    #    bounds on the fp32 result before rounding; bf16 == RNE(fp32)
     f32 = g["out_f32"][toks].astype(np.float64)
     max_f32, rms, mre_f32 = output_errors(f32, ref)
     out = g["out"][toks]
@@ -159,10 +180,18 @@ def run_case(inp, tokens=None, plan=None):
     excess = np.abs(out - ref) - bf16_half_ulp(ref)
     max_bf16, _, mre_bf16 = output_errors(out, ref)
     rep = dict(T=T, H=H, E=E, I=I, k=k, tokens=len(toks), near_tie_tokens=int(tie.sum()),
-               unique_experts=unique, rms_ref=rms, max_err_f32=max_f32, mean_rel_err_f32=mre_f32,
-               max_err_bf16=max_bf16, max_excess_over_half_ulp=float(excess.max()), mean_rel_err_bf16=mre_bf16)
+               exact_tie_tokens=int(exact.sum()), unique_experts=unique, rms_ref=rms,
+               max_err_bf16_over_rms=max_bf16 / rms if rms > 0 else 0.0, max_err_bf16=max_bf16,
+               mean_rel_err_bf16=mre_bf16, max_err_f32=max_f32, mean_rel_err_f32=mre_f32,
+               max_excess_over_half_ulp=float(excess.max()) if excess.size else 0.0)
+    # the bound is feasible in bf16 unless RNE-to-bf16 of the exact result already misses it
+    feasible = float(np.abs(bf16_rne(ref) - ref).max()) <= MAX_ERR_REL_RMS * rms if ref.size else True
+    rep["bf16_bound_feasible"] = feasible
+    if feasible:
+        assert max_bf16 <= MAX_ERR_REL_RMS * rms, rep
+    else:
+        assert bool(np.all(np.abs(out - ref) <= MAX_ERR_REL_RMS * rms + bf16_half_ulp(ref))), rep
+    assert mre_bf16 <= MEAN_REL_ERR, rep
     assert max_f32 <= MAX_ERR_REL_RMS * rms, rep
     assert mre_f32 <= MEAN_REL_ERR, rep
-    assert float(excess.max()) <= MAX_ERR_REL_RMS * rms, rep
-    assert mre_bf16 <= MEAN_REL_ERR, rep
     return rep
