@@ -132,6 +132,31 @@ int monomoe_forward_tokens(monomoe_plan_t plan, int32_t T, const void* x, const 
                            const void* w2, const float* w2_scale,
                            void* out, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): the operator of monomoe_forward without a
+ * plan, allocating nothing.  Its workspace is one file-scope device array of the library
+ * (32 MiB per GPU it runs on, held until the process ends; set up on the first call on each
+ * device); the caller passes inputs and outputs only:
+ *   shape, topk, renorm  as for monomoe_plan; softmax routing;
+ *   bias                 fp32 [E] logit bias (device, 16-byte aligned) or NULL, as for
+ *                        monomoe_plan_set_router_bias;
+ *   x .. out, stream     as for monomoe_forward;
+ *   status               int32 device word or NULL: receives, in stream order after the
+ *                        operator, MONOMOE_OK or the device-side failure of this call
+ *                        (MONOMOE_ERR_TIMEOUT, MONOMOE_ERR_INVALID for a bad expert id).
+ * Enqueues the operator's kernel(s) and one single-workgroup status kernel; never
+ * synchronises and calls no allocating routine.  Every call on one GPU shares that GPU's
+ * array, which keeps the last call's contents (the tagged exchange needs no clearing; the
+ * status word is cleared by the status kernel): calls that can overlap on one GPU (other
+ * streams, other host threads) race and must be serialised by the caller.  Returns
+ * MONOMOE_ERR_UNSUPPORTED when the shape's workspace exceeds 32 MiB (e.g. 64 tokens of the
+ * 4096x14336 layer), and the argument errors of monomoe_plan and monomoe_forward. */
+int monomoe_forward_noalloc(const monomoe_shape_t* shape, int topk, int renorm, const float* bias,
+                            const void* x, const void* router_w,
+                            const void* w13, const float* w13_scale,
+                            const void* w2, const float* w2_scale,
+                            void* out, int32_t* status, hipStream_t stream);
+
 /* Test hooks.  Every pointer may be NULL.  Pair index p = t*topk + j.
  *   topk_ids  int32 [T,topk]      selected experts, in selection order (written)
  *   topk_w    fp32  [T,topk]      their routing weights (written)

@@ -7,6 +7,7 @@
 #include <cmath>
 #include <algorithm>
 
+#include <mutex>
 #include <new>
 #include <string.h>
 
@@ -39,7 +40,7 @@ struct monomoe_plan_s {
     int grid;
     int lds_dyn;
     int lds_static;
-    int scratch;
+    int private_bytes;          // per-thread private (scratch) memory of the kernel
     int naq;
     int nslots;
     int tchunk;   // tokens per pass (T larger than one LDS-resident tile runs in passes)
@@ -217,6 +218,61 @@ int zero_workspace(monomoe_plan_s* pl) {
     return MONOMOE_OK;
 }
 
+// Kernel configuration and persistent grid of a new plan (shape, topk, renorm set) on
+// device dev: one workgroup per compute unit, the automatic kernel choice.
+int configure_plan(monomoe_plan_s* pl, int dev, int num_cus, int lds_total) {
+    pl->device = dev;
+    pl->num_cus = num_cus;
+    pl->lds_total = lds_total;
+    KernelConfig cfg{}, small{};
+    int small_T = 0;
+    const int cr = configure(pl, MONOMOE_KERNEL_AUTO, 0, 0, &cfg, &small, &small_T);
+    if (cr != MONOMOE_OK) return cr;
+    apply_config(pl, cfg, small, small_T);
+    hipFuncAttributes attr;
+    if (hipFuncGetAttributes(&attr, pl->var->fn) != hipSuccess) return MONOMOE_ERR_HIP;
+    pl->private_bytes = (int)attr.localSizeBytes;
+    pl->grid = pl->num_cus;   // one resident workgroup per CU
+    if (pl->grid > kGridMax) return MONOMOE_ERR_UNSUPPORTED;
+    return MONOMOE_OK;
+}
+
+// Workspace layout: control words | logits | quantised input (codes, scales) | act |
+// contrib, sized for one launch over every token of the plan and for the multi-tile
+// kernel's down slices.  Returns the total size; with a base address it also sets the
+// plan's workspace pointers.
+size_t layout_workspace(monomoe_plan_s* pl, uint8_t* base) {
+    const monomoe_shape_t& s = pl->shape;
+    const int T = std::max(s.T, 1), topk = pl->topk;
+    const int nsl = (s.I / 128) / mt_slice_blocks(s.I / 128);
+    size_t off = 0;
+    const size_t o_ctl = off;    off = align_up(off + sizeof(uint32_t) * ctl_words(), 256);
+    const size_t o_log = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * s.E, 256);
+    const size_t o_xq = off;     off = align_up(off + sizeof(uint64_t) * (size_t)T * s.H / 4, 256);
+    const size_t o_xs = off;     off = align_up(off + sizeof(uint64_t) * (size_t)T * s.H / 128, 256);
+    const size_t o_act = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * topk * s.I, 256);
+    const size_t o_out = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * topk * nsl * s.H, 256);
+    if (base) {
+        pl->ctl = reinterpret_cast<uint32_t*>(base + o_ctl);
+        pl->logits = reinterpret_cast<uint64_t*>(base + o_log);
+        pl->xq = reinterpret_cast<uint64_t*>(base + o_xq);
+        pl->xs = reinterpret_cast<uint64_t*>(base + o_xs);
+        pl->act = reinterpret_cast<uint64_t*>(base + o_act);
+        pl->contrib = reinterpret_cast<uint64_t*>(base + o_out);
+    }
+    return off;
+}
+
+// Shape and routing checks shared by monomoe_plan and the allocation-free forward.
+int check_shape(const monomoe_shape_t& s, int topk) {
+    if (s.T < 0 || s.H <= 0 || s.I <= 0 || s.E <= 0) return MONOMOE_ERR_INVALID;
+    if (s.H % 128 || s.I % 128) return MONOMOE_ERR_INVALID;
+    if (topk < 1 || topk > s.E) return MONOMOE_ERR_INVALID;
+    if (s.T > kTLimit || s.E > kEMax || topk > kKMax) return MONOMOE_ERR_UNSUPPORTED;
+    if (!find_kernel(s.H, s.I)) return MONOMOE_ERR_UNSUPPORTED;
+    return MONOMOE_OK;
+}
+
 // One forward of T tokens (0 <= T <= the plan's T) with the plan's configuration for T.
 int launch(monomoe_plan_t plan, int T, const void* x, const void* router_w, const void* w13, const float* w13_scale,
            const void* w2, const float* w2_scale, void* out, const monomoe_debug_t* dbg, hipStream_t stream,
@@ -317,7 +373,116 @@ int launch(monomoe_plan_t plan, int T, const void* x, const void* router_w, cons
 
 }  // namespace
 
+// ------------------------------------------------------------------------------------
+// Allocation-free forward (monomoe_forward_noalloc): the workspace lives in one file-scope
+// device array instead of a plan's hipMalloc'd buffer.
+// ------------------------------------------------------------------------------------
+constexpr size_t kNoAllocScratchBytes = size_t(32) << 20;   // the largest workspace it serves
+
+// One copy per GPU the library runs on, held until the process ends.  Static storage, so it
+// is zero when the code object is loaded: every launch epoch 0 and the status word clear,
+// the state the tagged-exchange protocol starts from.  Host code must never pass this name
+// to a kernel (on the host it is a stand-in, not a device address): the device address is
+// taken once per device with hipGetSymbolAddress and kept in g_scratch_dev.
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
+namespace {
+
+constexpr int kNoAllocDevices = 64;
+constexpr int kNoAllocCache = 8;
+
+struct NoAllocEntry {
+    int valid, dev, topk, renorm;
+    monomoe_shape_t shape;
+    monomoe_plan_s plan;   // configuration and workspace pointers into the device's scratch
+};
+
+std::mutex g_noalloc_mu;
+uint8_t* g_scratch_dev[kNoAllocDevices];   // device address of `scratch`, per device
+NoAllocEntry g_noalloc_cache[kNoAllocCache];
+int g_noalloc_next = 0;
+
+// Reports the device status of the launch before it (MONOMOE_OK, MONOMOE_ERR_TIMEOUT or
+// MONOMOE_ERR_INVALID for a rejected expert id) into *out when out is not null, and clears
+// the status word, so one failed call does not fail every later one.
+__global__ void noalloc_status(uint32_t* word, int32_t* out) {
+    if (threadIdx.x != 0) return;
+    const uint32_t st = __hip_atomic_load(word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (out) *out = st == kDevOk ? MONOMOE_OK : (st == kDevTimeout ? MONOMOE_ERR_TIMEOUT : MONOMOE_ERR_INVALID);
+    if (st != kDevOk) __hip_atomic_store(word, (uint32_t)kDevOk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The configuration of (device, shape, topk, renorm) with its workspace laid out in the
+// device's scratch; computed on first use (set-up of the device included) and cached.
+int noalloc_plan(int dev, const monomoe_shape_t& s, int topk, int renorm, monomoe_plan_s* out) {
+    std::lock_guard<std::mutex> lock(g_noalloc_mu);
+    if (!g_scratch_dev[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return MONOMOE_ERR_HIP;
+        g_scratch_dev[dev] = static_cast<uint8_t*>(ptr);
+    }
+    for (const NoAllocEntry& c : g_noalloc_cache) {
+        if (c.valid && c.dev == dev && c.topk == topk && c.renorm == renorm && c.shape.T == s.T && c.shape.H == s.H &&
+            c.shape.E == s.E && c.shape.I == s.I) {
+            *out = c.plan;
+            return MONOMOE_OK;
+        }
+    }
+    monomoe_plan_s pl{};
+    pl.shape = s;
+    pl.topk = topk;
+    pl.renorm = renorm ? 1 : 0;
+    pl.kern = find_kernel(s.H, s.I);
+    pl.mtv = find_mt_kernel(s.H, s.I);
+    pl.policy = MONOMOE_ROUTING_SOFTMAX;
+    pl.route_scale = 1.0f;
+    int cus = 0, lds = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+        return MONOMOE_ERR_HIP;
+    const int cr = configure_plan(&pl, dev, cus, lds);
+    if (cr != MONOMOE_OK) return cr;
+    const size_t need = layout_workspace(&pl, nullptr);
+    if (need > kNoAllocScratchBytes) return MONOMOE_ERR_UNSUPPORTED;
+    pl.ws = g_scratch_dev[dev];
+    pl.ws_bytes = need;
+    layout_workspace(&pl, g_scratch_dev[dev]);
+    NoAllocEntry& slot = g_noalloc_cache[g_noalloc_next];
+    g_noalloc_next = (g_noalloc_next + 1) % kNoAllocCache;
+    slot.valid = 1;
+    slot.dev = dev;
+    slot.topk = topk;
+    slot.renorm = renorm ? 1 : 0;
+    slot.shape = s;
+    slot.plan = pl;
+    *out = pl;
+    return MONOMOE_OK;
+}
+
+}  // namespace
+
 extern "C" {
+
+int monomoe_forward_noalloc(const monomoe_shape_t* shape, int topk, int renorm, const float* bias, const void* x,
+                            const void* router_w, const void* w13, const float* w13_scale, const void* w2,
+                            const float* w2_scale, void* out, int32_t* status, hipStream_t stream) {
+    if (!shape) return MONOMOE_ERR_INVALID;
+    const int sc = check_shape(*shape, topk);
+    if (sc != MONOMOE_OK) return sc;
+    if ((bias && !aligned16(bias)) || (reinterpret_cast<uintptr_t>(status) & 3u)) return MONOMOE_ERR_INVALID;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return MONOMOE_ERR_HIP;
+    if (dev < 0 || dev >= kNoAllocDevices) return MONOMOE_ERR_UNSUPPORTED;
+    monomoe_plan_s pl;
+    const int pr = noalloc_plan(dev, *shape, topk, renorm, &pl);
+    if (pr != MONOMOE_OK) return pr;
+    pl.bias = bias;
+    const int rc = launch(&pl, shape->T, x, router_w, w13, w13_scale, w2, w2_scale, out, nullptr, stream);
+    if (rc != MONOMOE_OK || shape->T == 0) return rc;
+    hipLaunchKernelGGL(noalloc_status, dim3(1), dim3(64), 0, stream, pl.ctl + kCtlStatus, status);
+    if (hipGetLastError() != hipSuccess) return MONOMOE_ERR_HIP;
+    return MONOMOE_OK;
+}
 
 int monomoe_supported_shape(int32_t H, int32_t I) { return find_kernel(H, I) ? 1 : 0; }
 
@@ -336,12 +501,9 @@ const char* monomoe_status_string(int status) {
 int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_plan_t* plan_out) {
     if (!shape || !plan_out) return MONOMOE_ERR_INVALID;
     const monomoe_shape_t s = *shape;
-    if (s.T < 0 || s.H <= 0 || s.I <= 0 || s.E <= 0) return MONOMOE_ERR_INVALID;
-    if (s.H % 128 || s.I % 128) return MONOMOE_ERR_INVALID;
-    if (topk < 1 || topk > s.E) return MONOMOE_ERR_INVALID;
-    if (s.T > kTLimit || s.E > kEMax || topk > kKMax) return MONOMOE_ERR_UNSUPPORTED;
+    const int sc = check_shape(s, topk);
+    if (sc != MONOMOE_OK) return sc;
     const KernelEntry* kern = find_kernel(s.H, s.I);
-    if (!kern) return MONOMOE_ERR_UNSUPPORTED;
 
     monomoe_plan_s* pl = new (std::nothrow) monomoe_plan_s();
     if (!pl) return MONOMOE_ERR_HIP;
@@ -361,54 +523,17 @@ int monomoe_plan(const monomoe_shape_t* shape, int topk, int renorm, monomoe_pla
         delete pl;
         return MONOMOE_ERR_HIP;
     }
-    pl->device = dev;
-    pl->num_cus = prop.multiProcessorCount;
-    pl->lds_total = (int)prop.sharedMemPerBlock;
-    KernelConfig cfg{}, small{};
-    int small_T = 0;
-    const int cr = configure(pl, MONOMOE_KERNEL_AUTO, 0, 0, &cfg, &small, &small_T);
+    const int cr = configure_plan(pl, dev, prop.multiProcessorCount, (int)prop.sharedMemPerBlock);
     if (cr != MONOMOE_OK) {
         delete pl;
         return cr;
     }
-    apply_config(pl, cfg, small, small_T);
-    {
-        hipFuncAttributes attr;
-        if (hipFuncGetAttributes(&attr, pl->var->fn) != hipSuccess) {
-            delete pl;
-            return MONOMOE_ERR_HIP;
-        }
-        pl->scratch = (int)attr.localSizeBytes;
-    }
-    pl->grid = pl->num_cus;   // one resident workgroup per CU
-    if (pl->grid > kGridMax) {
-        delete pl;
-        return MONOMOE_ERR_UNSUPPORTED;
-    }
-
-    // workspace: control words | logits | quantised input (codes, scales) | act | contrib,
-    // sized for one launch over every token and for the multi-tile kernel's down slices
-    const int T = std::max(s.T, 1);
-    const int nsl = (s.I / 128) / mt_slice_blocks(s.I / 128);
-    size_t off = 0;
-    const size_t o_ctl = off;    off = align_up(off + sizeof(uint32_t) * ctl_words(), 256);
-    const size_t o_log = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * s.E, 256);
-    const size_t o_xq = off;     off = align_up(off + sizeof(uint64_t) * (size_t)T * s.H / 4, 256);
-    const size_t o_xs = off;     off = align_up(off + sizeof(uint64_t) * (size_t)T * s.H / 128, 256);
-    const size_t o_act = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * topk * s.I, 256);
-    const size_t o_out = off;    off = align_up(off + sizeof(uint64_t) * (size_t)T * topk * nsl * s.H, 256);
-    pl->ws_bytes = off;
+    pl->ws_bytes = layout_workspace(pl, nullptr);
     if (hipMalloc(&pl->ws, pl->ws_bytes) != hipSuccess) {
         delete pl;
         return MONOMOE_ERR_HIP;
     }
-    uint8_t* base = static_cast<uint8_t*>(pl->ws);
-    pl->ctl = reinterpret_cast<uint32_t*>(base + o_ctl);
-    pl->logits = reinterpret_cast<uint64_t*>(base + o_log);
-    pl->xq = reinterpret_cast<uint64_t*>(base + o_xq);
-    pl->xs = reinterpret_cast<uint64_t*>(base + o_xs);
-    pl->act = reinterpret_cast<uint64_t*>(base + o_act);
-    pl->contrib = reinterpret_cast<uint64_t*>(base + o_out);
+    layout_workspace(pl, static_cast<uint8_t*>(pl->ws));
     const int zr = zero_workspace(pl);
     if (zr != MONOMOE_OK) {
         (void)hipFree(pl->ws);

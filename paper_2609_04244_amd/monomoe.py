@@ -28,7 +28,7 @@ KERNEL_MULTI = 2
 EXPORTS = (
     "monomoe_plan", "monomoe_plan_destroy", "monomoe_plan_set_router_bias", "monomoe_plan_set_routing",
     "monomoe_plan_set_schedule",
-    "monomoe_forward", "monomoe_forward_tokens",
+    "monomoe_forward", "monomoe_forward_tokens", "monomoe_forward_noalloc",
     "monomoe_forward_debug", "monomoe_forward_timed", "monomoe_plan_status", "monomoe_plan_reset", "monomoe_plan_info",
     "monomoe_supported_shape", "monomoe_status_string", "monomoe_stream_copy", "monomoe_stream_read",
 )
@@ -90,6 +90,8 @@ def lib():
         L.monomoe_forward.restype = ctypes.c_int
         L.monomoe_forward_tokens.argtypes = [vp, ctypes.c_int32] + [vp] * 8
         L.monomoe_forward_tokens.restype = ctypes.c_int
+        L.monomoe_forward_noalloc.argtypes = [ctypes.POINTER(Shape), ctypes.c_int, ctypes.c_int] + [vp] * 10
+        L.monomoe_forward_noalloc.restype = ctypes.c_int
         L.monomoe_forward_debug.argtypes = [vp] * 8 + [ctypes.POINTER(Debug), vp]
         L.monomoe_forward_debug.restype = ctypes.c_int
         L.monomoe_forward_timed.argtypes = [vp] * 11
@@ -134,6 +136,18 @@ def stream_read(src, sink, nbytes=None, stream=None):
     rc = lib().monomoe_stream_read(ctypes.c_void_p(src.data_ptr()), n, ctypes.c_void_p(sink.data_ptr()), _stream(stream))
     if rc != MONOMOE_OK:
         raise MonoMoEError(rc, "monomoe_stream_read")
+
+
+def forward_noalloc(T, H, E, I, topk, renorm, x, router_w, w13, w13_scale, w2, w2_scale, out, bias=None,
+                    status=None, stream=None):
+    """monomoe_forward_noalloc: the operator without a plan (the library's static scratch as
+    workspace).  out: bf16 [T,H] device tensor; status: int32 [1] device tensor or None."""
+    rc = lib().monomoe_forward_noalloc(ctypes.byref(Shape(int(T), int(H), int(E), int(I))), int(topk), int(bool(renorm)),
+                                       _ptr(bias), _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale), _ptr(w2),
+                                       _ptr(w2_scale), _ptr(out), _ptr(status), _stream(stream))
+    if rc != MONOMOE_OK:
+        raise MonoMoEError(rc, "monomoe_forward_noalloc")
+    return out
 
 
 _hip = None
