@@ -1,24 +1,35 @@
 #!/usr/bin/env python3
 """Benchmark of the fused routed-MoE decode operator on one MI355X.
 
-One step = one forward of the operator for each decode token count T in {1, 2, 4, 8} on
-the small-expert layer shape (H=2048, E=128, I=768, top-8, renormalised softmax), each
-forward on its own synthetic layer.  Layers rotate over `--layers` distinct weight sets
-so that successive launches stream weights from HBM rather than from the 256 MB
-last-level cache (as consecutive MoE layers of a decode step do).
+One step = one forward of the operator for each decode token count T in {1, 2, 4, 8}; each of
+the evaluated layers is timed in its own block of steps (the paper's isolated-operator
+protocol, consecutive launches of one operator):
+  wide_fine         H=7168 E=256 I=2048 top-8, renormalised softmax (the headline: the largest
+                    evaluated layer that fits one GPU, ~11 GB of FP8 expert weights),
+  small_expert      H=2048 E=128 I=768  top-8, renormalised softmax,
+  many_tiny_expert  H=2048 E=256 I=512  top-8, renormalised softmax with a per-expert logit
+                    bias (the paper's Qwen3.5-35B-A3B per-GPU shape).
+Every layer rotates over enough distinct synthetic weight sets that the weights a launch reads
+were last read more than 512 MB of weight traffic earlier (twice the 256 MB last-level cache),
+so every launch streams its weights from HBM, as consecutive MoE layers of a decode step do.
 
 Each launch's duration comes from HIP events that its own dispatch stamps (hipExtLaunchKernel
 through monomoe_forward_timed): the kernel's begin and end, as a kernel trace reports them.
+Each (layer, T) forward is also captured into a HIP graph and its replays are event-timed on
+the stream (the paper's protocol: graph replays after warm-ups), reported beside the kernel
+time.
 
-Printed (one JSON line): value = algorithmic bytes of the step / summed launch time (GB/s);
-per-T latency (mean and p50, microseconds), achieved GB/s and fraction of the 8 TB/s peak;
-a roofline object for the kernel; and the CPU oracle timed on a bounded sample.
+Printed (one JSON line): value = algorithmic bytes / summed launch time (GB/s) of the headline
+layer over its token counts; per-T latency (mean, p10/p50/p90, graph replay p50), achieved GB/s
+and fraction of the 8 TB/s peak; the same block for every layer under "workloads"; a roofline
+object for the headline kernel; the CPU oracle on a bounded sample of the headline layer, on
+one host core and on all of them.
 
 Other layers and token counts (up to 64, where the multi-tile kernel runs) are a flag away:
-`--workload coarse --tokens 16,32,64`; the workload's routing policy (softmax, or sigmoid
-with a selection bias) is applied to every plan.  The roofline's measured traffic is the
-committed FETCH_SIZE/WRITE_SIZE record of each T's kernel on that workload, when there is
-one and its kernel sources are unchanged.
+`--workloads coarse --tokens 16,32,64`; each layer's routing policy (softmax, or sigmoid with a
+selection bias) is applied to its plans.  A workload's measured traffic is the committed
+FETCH_SIZE/WRITE_SIZE record of each T's kernel on that workload, when there is one and its
+kernel sources are unchanged.
 
 Algorithmic bytes of one launch: every selected expert's weights read once,
 U * 3*H*I fp8 bytes plus their fp32 block scales U * 3*H*I/4096, plus the router
@@ -26,6 +37,7 @@ weight E*H*2, the input T*H*2 and the output T*H*2 bytes.
 """
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -34,7 +46,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0
-TS = (1, 2, 4, 8)
+DEFAULT_WORKLOADS = "wide_fine,small_expert,many_tiny_expert"
+REUSE_BYTES = 512e6       # weight bytes between two reads of the same weights, at least
+LAYER_BUDGET = 40e9       # device bytes of generated layers per workload, at most
 # HBM counter records (rocprofv3 FETCH_SIZE / WRITE_SIZE passes over the C++ profiling
 # driver, calibrated on a plain copy kernel), one per kernel and workload; a record is used
 # only while its kernel's sources still hash to the value it was taken on.
@@ -46,13 +60,16 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="small_expert")
+    ap.add_argument("--workloads", default=DEFAULT_WORKLOADS,
+                    help="comma-separated layers; the first is the headline")
+    ap.add_argument("--workload", help="a single layer (same as --workloads NAME)")
     ap.add_argument("--tokens", default="1,2,4,8",
                     help="decode token counts of one step (up to 64; the metric is quoted on 1,2,4,8)")
-    ap.add_argument("--layers", type=int, default=16)
+    ap.add_argument("--layers", type=int, default=0, help="weight sets per workload (0: as the reuse bound needs)")
+    ap.add_argument("--replays", type=int, default=100, help="timed graph replays per (layer, T); 0: none")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="per oracle mode (one core, all cores)")
     return ap.parse_args()
 
 
@@ -64,7 +81,17 @@ def algorithmic_bytes(U, T, H, E, I):
     return weights + scales + E * H * 2 + 2 * T * H * 2
 
 
-def measured_traffic(workload, kinds):
+def layers_needed(cfg, TS, expected_unique):
+    """Distinct weight sets so that, with the launches of all token counts rotating over them,
+    a launch's weights were last read at least REUSE_BYTES of weight traffic earlier."""
+    H, E, I, k = cfg["H"], cfg["E"], cfg["I"], cfg["k"]
+    smallest = min(expected_unique(E, k, T) for T in TS) * 3 * H * I
+    n = int(math.ceil(REUSE_BYTES / smallest)) + 1
+    layer_bytes = E * 3 * H * I
+    return max(2, min(n, int(LAYER_BUDGET // layer_bytes)))
+
+
+def measured_traffic(workload, kinds, TS):
     """HBM bytes per launch (read + write, mean over the step's token counts) from the
     committed counter records, or None unless every token count T has a record of this
     workload, taken on the kernel that runs at T (kinds[T], "single" or "multi") whose
@@ -86,6 +113,165 @@ def measured_traffic(workload, kinds):
     return sum(per[T] for T in TS) / len(TS)
 
 
+class Workload:
+    """The generated layers, plans, outputs and per-launch records of one layer shape."""
+
+    def __init__(self, name, TS, n_layers, seed, dev):
+        import torch
+        from paper_2609_04244_amd import monomoe as mm
+        from paper_2609_04244_amd import workloads as wl
+        self.name, self.TS = name, TS
+        self.cfg = cfg = wl.config(name)
+        self.H, self.E, self.I, self.k, self.renorm = cfg["H"], cfg["E"], cfg["I"], cfg["k"], cfg["renorm"]
+        self.n = n_layers or layers_needed(cfg, TS, wl.expected_unique_experts)
+        print("bench: generating %d layers of %s" % (self.n, name), file=sys.stderr, flush=True)
+        self.layers = [wl.generate(cfg, T=max(TS), seed=seed + 1000 * l, device=dev) for l in range(self.n)]
+        self.plans = {T: mm.Plan(T, self.H, self.E, self.I, self.k, self.renorm) for T in TS}
+        self.outs = {T: torch.empty((T, self.H), dtype=torch.bfloat16, device=dev) for T in TS}
+        self.xs = {(l, T): self.layers[l]["x"][:T].contiguous() for l in range(self.n) for T in TS}
+        # one rotation per workload over all of its launches, so that consecutive launches (of
+        # any T) read different weight sets
+        self.next_layer = 0
+        self.records = {T: [] for T in TS}   # (layer, timer, timed?)
+        self.graph_ms = {T: [] for T in TS}
+        self.U = {}
+
+    def route(self, T, L):   # the layer's routing inputs (logit bias; sigmoid selection bias)
+        from paper_2609_04244_amd import monomoe as mm
+        p = self.plans[T]
+        if L["bias"] is not None:
+            p.set_router_bias(L["bias"])
+        if L["policy"] == "sigmoid_bias":
+            p.set_routing(mm.ROUTING_SIGMOID_BIAS, L["sel_bias"], L["route_scale"])
+
+    def args(self, l, T):
+        L = self.layers[l]
+        return (self.xs[(l, T)], L["router_w"], L["w13"], L["w13_scale"], L["w2"], L["w2_scale"])
+
+    def select(self):
+        """Unique experts of every (layer, T), from the operator's own selection (untimed)."""
+        import torch
+        from paper_2609_04244_amd import monomoe as mm
+        for l in range(self.n):
+            for T in self.TS:
+                self.route(T, self.layers[l])
+                _, d = self.plans[T].forward_debug(*self.args(l, T))
+                torch.cuda.synchronize()
+                self.U[(l, T)] = len(set(d["ids"].cpu().numpy().reshape(-1).tolist()))
+        for T in self.TS:
+            if self.plans[T].status() != mm.MONOMOE_OK:
+                raise RuntimeError("%s: device status after the selection pass: %s"
+                                   % (self.name, mm.status_string(self.plans[T].status())))
+
+    def launch(self, T, timed):
+        from paper_2609_04244_amd import monomoe as mm
+        l = self.next_layer
+        self.next_layer = (l + 1) % self.n
+        self.route(T, self.layers[l])
+        timer = mm.DispatchTimer()
+        self.plans[T].forward_timed(*self.args(l, T), self.outs[T], timer)
+        self.records[T].append((l, timer, timed))
+
+    def capture_graphs(self):
+        """One HIP graph per (layer, T), each replaying that layer's forward."""
+        import torch
+        self.graphs = {}
+        side = torch.cuda.Stream()
+        for T in self.TS:
+            for l in range(self.n):
+                self.route(T, self.layers[l])   # the routing inputs are read from the plan at capture
+                side.wait_stream(torch.cuda.current_stream())
+                with torch.cuda.stream(side):
+                    self.plans[T].forward(*self.args(l, T), out=self.outs[T])
+                torch.cuda.current_stream().wait_stream(side)
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g):
+                    self.plans[T].forward(*self.args(l, T), out=self.outs[T], check=False)
+                self.graphs[(l, T)] = g
+        torch.cuda.synchronize()
+
+    def replay(self, T, timed):
+        import torch
+        l = self.next_layer
+        self.next_layer = (l + 1) % self.n
+        if not timed:
+            self.graphs[(l, T)].replay()
+            return None
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        self.graphs[(l, T)].replay()
+        b.record()
+        return (a, b)
+
+    def status_ok(self):
+        from paper_2609_04244_amd import monomoe as mm
+        for T in self.TS:
+            st = self.plans[T].status()
+            if st != mm.MONOMOE_OK:
+                raise RuntimeError("%s: device status after timing: %s" % (self.name, mm.status_string(st)))
+
+    def summary(self, steps):
+        import numpy as np
+        from paper_2609_04244_amd import workloads as wl
+        H, E, I, k = self.H, self.E, self.I, self.k
+        per_T = {}
+        tot_bytes = tot_ms = 0.0
+        for T in self.TS:
+            ms, by, wb = [], [], []
+            for l, timer, timed in self.records[T]:
+                if not timed:
+                    continue
+                ms.append(timer.elapsed_ms())
+                u = self.U[(l, T)]
+                by.append(algorithmic_bytes(u, T, H, E, I))
+                wb.append(u * 3 * H * I)
+            ms = np.array(ms)
+            by = np.array(by, dtype=np.float64)
+            gbps = by.sum() / (ms.sum() * 1e-3) / 1e9
+            e = {
+                "us_mean": round(float(ms.mean() * 1e3), 2), "us_p50": round(float(np.median(ms) * 1e3), 2),
+                "us_p10": round(float(np.percentile(ms, 10) * 1e3), 2),
+                "us_p90": round(float(np.percentile(ms, 90) * 1e3), 2),
+                "unique_experts_mean": round(float(np.mean([self.U[(l, T)] for l in range(self.n)])), 2),
+                "unique_experts_uniform_estimate": round(wl.expected_unique_experts(E, k, T), 2),
+                "GBps": round(float(gbps), 1), "frac_of_peak": round(float(gbps / PEAK_HBM_GBPS), 4),
+                "expert_weight_GBps": round(float(np.sum(wb) / (ms.sum() * 1e-3) / 1e9), 1),
+            }
+            if self.graph_ms[T]:
+                g = np.array(self.graph_ms[T])
+                e["graph_replay_us_p50"] = round(float(np.median(g) * 1e3), 2)
+                e["graph_replay_us_p10"] = round(float(np.percentile(g, 10) * 1e3), 2)
+                e["graph_replay_us_p90"] = round(float(np.percentile(g, 90) * 1e3), 2)
+            per_T[str(T)] = e
+            tot_bytes += by.sum()
+            tot_ms += ms.sum()
+        value = tot_bytes / (tot_ms * 1e-3) / 1e9
+        kinds = {T: "multi" if self.plans[T].info()["multi_tile"] else "single" for T in self.TS}
+        traffic = measured_traffic(self.name, kinds, self.TS)
+        cfg = self.cfg
+        routing = ("sigmoid routing with selection bias" if cfg.get("policy") == "sigmoid_bias" else
+                   ("renormalised" if self.renorm else "plain") + " softmax") + \
+            (" + per-expert logit bias" if cfg.get("bias_std") else "")
+        n_launch = steps * len(self.TS)
+        return {
+            "layer": "%s: H=%d E=%d I=%d top-%d %s, block-FP8 128x128 weights, T in %s, %d rotated weight sets" % (
+                self.name, H, E, I, k, routing, list(self.TS), self.n),
+            "value_GBps": round(float(value), 1), "frac_of_peak": round(float(value / PEAK_HBM_GBPS), 4),
+            "launch_us_mean": round(float(tot_ms / n_launch * 1e3), 2),
+            "ms_per_step": round(float(self.ms_per_step), 4),
+            "algorithmic_bytes_per_launch": round(float(tot_bytes / n_launch)),
+            "traffic": None if traffic is None else round(float(traffic)),
+            "kernel": ", ".join(sorted({"monomoe_fused%s<%d,%d>" % ("_mt" if self.plans[T].info()["multi_tile"] else "",
+                                                                    H, I) for T in self.TS})),
+            "per_T": per_T,
+        }, value, tot_bytes, tot_ms
+
+    def close(self):
+        for p in self.plans.values():
+            p.close()
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -93,205 +279,189 @@ def main():
               "(--gpus %d requested)" % args.gpus, file=sys.stderr, flush=True)
         sys.exit(2)
 
-    import numpy as np
     import torch
-    from paper_2609_04244_amd import monomoe as mm
-    from paper_2609_04244_amd import workloads as wl
 
-    global TS
     TS = tuple(int(t) for t in args.tokens.split(","))
-    cfg = wl.config(args.workload)
-    H, E, I, k, renorm = cfg["H"], cfg["E"], cfg["I"], cfg["k"], cfg["renorm"]
+    names = [args.workload] if args.workload else args.workloads.split(",")
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    print("bench: generating %d layers of %s" % (args.layers, args.workload), file=sys.stderr, flush=True)
-    layers = [wl.generate(cfg, T=max(TS), seed=args.seed + 1000 * l, device=dev) for l in range(args.layers)]
-    plans = {T: mm.Plan(T, H, E, I, k, renorm) for T in TS}
-    outs = {T: torch.empty((T, H), dtype=torch.bfloat16, device=dev) for T in TS}
-    xs = {(l, T): layers[l]["x"][:T].contiguous() for l in range(args.layers) for T in TS}
+    wls = [Workload(n, TS, args.layers, args.seed, dev) for n in names]
+    for w in wls:
+        w.select()
 
-    def route(p, L):   # the layer's routing inputs (logit bias; sigmoid selection bias)
-        if L["bias"] is not None:
-            p.set_router_bias(L["bias"])
-        if L["policy"] == "sigmoid_bias":
-            p.set_routing(mm.ROUTING_SIGMOID_BIAS, L["sel_bias"], L["route_scale"])
-
-    def launch(l, T, timer):
-        L = layers[l]
-        p = plans[T]
-        route(p, L)
-        p.forward_timed(xs[(l, T)], L["router_w"], L["w13"], L["w13_scale"], L["w2"], L["w2_scale"], outs[T], timer)
-
-    # unique experts of every (layer, T), from the operator's own selection (untimed)
-    U = {}
-    for l in range(args.layers):
-        for T in TS:
-            L = layers[l]
-            route(plans[T], L)
-            _, d = plans[T].forward_debug(xs[(l, T)], L["router_w"], L["w13"], L["w13_scale"], L["w2"],
-                                          L["w2_scale"])
-            torch.cuda.synchronize()
-            U[(l, T)] = len(set(d["ids"].cpu().numpy().reshape(-1).tolist()))
-    for T in TS:
-        if plans[T].status() != mm.MONOMOE_OK:
-            raise RuntimeError("device status after the selection pass: %s" % mm.status_string(plans[T].status()))
-
+    # dispatch-stamped kernel times, one layer after the other (the paper's isolated-operator
+    # protocol: consecutive launches of one operator shape); a step is one launch per T
     stream = torch.cuda.current_stream()
-    order = [(s, T) for s in range(args.warmup + args.steps) for T in TS]
-    n_launch = len(order)
-    # each launch's dispatch stamps its own begin and end (hipExtLaunchKernel events)
-    timers = [mm.DispatchTimer() for _ in range(n_launch)]
-    layer_of = []
-    li = 0
-    for i in range(n_launch):
-        layer_of.append(li % args.layers)
-        li += 1
+    wall = 0.0
+    ms_per_step = 0.0
+    for w in wls:
+        torch.cuda.synchronize()
+        w_start = torch.cuda.Event(enable_timing=True)
+        w_end = torch.cuda.Event(enable_timing=True)
+        t_start = None
+        for s in range(args.warmup + args.steps):
+            if s == args.warmup:
+                torch.cuda.synchronize()
+                t_start = time.perf_counter()
+                w_start.record(stream)
+            for T in TS:
+                w.launch(T, s >= args.warmup)
+        w_end.record(stream)
+        torch.cuda.synchronize()
+        wall += time.perf_counter() - t_start
+        w.status_ok()
+        w.ms_per_step = w_start.elapsed_time(w_end) / args.steps
+        ms_per_step += w.ms_per_step
 
-    torch.cuda.synchronize()
-    t_start = None
-    w_start = torch.cuda.Event(enable_timing=True)
-    w_end = torch.cuda.Event(enable_timing=True)
-    for i, (s, T) in enumerate(order):
-        if s == args.warmup and t_start is None:
+    # graph replays, event-timed on the stream, same order and layer rotation
+    if args.replays > 0:
+        for w in wls:
+            w.capture_graphs()
+            pending = []
+            for r in range(20 + args.replays):
+                for T in TS:
+                    ev = w.replay(T, r >= 20)
+                    if ev is not None:
+                        pending.append((T, ev))
             torch.cuda.synchronize()
-            t_start = time.perf_counter()
-            w_start.record(stream)
-        launch(layer_of[i], T, timers[i])
-    w_end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_start
-    for T in TS:
-        st = plans[T].status()
-        if st != mm.MONOMOE_OK:
-            raise RuntimeError("device status after timing: %s" % mm.status_string(st))
+            for T, (a, b) in pending:
+                w.graph_ms[T].append(a.elapsed_time(b))
+            w.status_ok()
 
-    per_T = {}
-    tot_bytes = 0.0
-    tot_ms = 0.0
-    wbytes_tot = 0.0
-    for T in TS:
-        ms, by, wb = [], [], []
-        for i, (s, TT) in enumerate(order):
-            if s < args.warmup or TT != T:
-                continue
-            ms.append(timers[i].elapsed_ms())
-            u = U[(layer_of[i], T)]
-            by.append(algorithmic_bytes(u, T, H, E, I))
-            wb.append(u * 3 * H * I)
-        ms = np.array(ms)
-        by = np.array(by, dtype=np.float64)
-        gbps = by.sum() / (ms.sum() * 1e-3) / 1e9
-        per_T[str(T)] = {
-            "us_mean": round(float(ms.mean() * 1e3), 2), "us_p50": round(float(np.median(ms) * 1e3), 2),
-            "us_p10": round(float(np.percentile(ms, 10) * 1e3), 2),
-            "us_p90": round(float(np.percentile(ms, 90) * 1e3), 2),
-            "unique_experts_mean": round(float(np.mean([U[(l, T)] for l in range(args.layers)])), 2),
-            "unique_experts_uniform_estimate": round(wl.expected_unique_experts(E, k, T), 2),
-            "GBps": round(float(gbps), 1), "frac_of_peak": round(float(gbps / PEAK_HBM_GBPS), 4),
-            "expert_weight_GBps": round(float(np.sum(wb) / (ms.sum() * 1e-3) / 1e9), 1),
-        }
-        tot_bytes += by.sum()
-        tot_ms += ms.sum()
-        wbytes_tot += float(np.sum(wb))
-    value = tot_bytes / (tot_ms * 1e-3) / 1e9
-    ms_per_step = w_start.elapsed_time(w_end) / args.steps
-    kinds = {T: "multi" if plans[T].info()["multi_tile"] else "single" for T in TS}
-    traffic = measured_traffic(args.workload, kinds)
-
+    blocks = {}
+    head = None
+    for w in wls:
+        blk, value, tot_bytes, tot_ms = w.summary(args.steps)
+        blocks[w.name] = blk
+        if head is None:
+            head = (w, blk, value)
+    w0, blk0, value = head
     res = {
         "metric": "routed-MoE op latency us + achieved HBM GB/s (% of peak) at T=" + ",".join(map(str, TS)) + " tokens",
         "value": round(float(value), 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(float(ms_per_step), 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "fp8_e4m3 (fp32 accumulate)", "data": "synthetic",
+        "scaling": "weak", "vs_baseline": None, "dtype": "fp8_e4m3 operands (exact fp16 MFMA), fp32 accumulate",
+        "data": "synthetic",
         "config": {
-            "workload": "%s: H=%d E=%d I=%d top-%d %s, block-FP8 128x128 weights, T in %s, "
-                        "%d rotated layers" % (args.workload, H, E, I, k,
-                                               "sigmoid routing with selection bias"
-                                               if cfg.get("policy") == "sigmoid_bias" else
-                                               ("renormalised" if renorm else "plain") + " softmax",
-                                               list(TS), args.layers),
-            "launches_per_step": len(TS), "grid": plans[TS[0]].info()["grid"],
-            "block": plans[TS[0]].info()["block"],
+            "workload": blk0["layer"],
+            "other_workloads": [b["layer"] for n, b in blocks.items() if n != w0.name],
+            "launches_per_step": len(TS) * len(wls), "grid": w0.plans[TS[0]].info()["grid"],
+            "block": w0.plans[TS[0]].info()["block"],
+            "step": "one forward per token count; each layer is timed in its own block of steps; value, per_T and "
+                    "roofline are the headline layer's; ms_per_step sums one step of every layer",
         },
-        "per_T": per_T,
+        "per_T": blk0["per_T"],
+        "workloads": blocks,
         "roofline": {
             "bound": "hbm", "achieved": round(float(value), 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
             "frac": round(float(value / PEAK_HBM_GBPS), 4),
-            "traffic": None if traffic is None else round(float(traffic)),
+            "traffic": blk0["traffic"],
             "traffic_unit": "HBM bytes per launch (read + write, mean over T)",
-            "algorithmic_bytes_per_launch": round(float(tot_bytes / (args.steps * len(TS)))),
-            "kernel": ", ".join(sorted({"monomoe_fused%s<%d,%d>" % ("_mt" if plans[T].info()["multi_tile"] else "", H, I)
-                                        for T in TS})),
-            "launch_us_mean": round(float(tot_ms / (args.steps * len(TS)) * 1e3), 2),
+            "algorithmic_bytes_per_launch": blk0["algorithmic_bytes_per_launch"],
+            "kernel": blk0["kernel"],
+            "launch_us_mean": blk0["launch_us_mean"],
         },
         "wall_s_timed": round(wall, 3),
     }
-
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(args, layers, U, plans, outs, xs, cfg, wbytes_tot / args.steps,
-                                           tot_bytes / args.steps)
-    for p in plans.values():
-        p.close()
+        res["cpu_baseline"] = cpu_baseline(args, w0, TS)
+    for w in wls:
+        w.close()
     print(json.dumps(res), flush=True)
 
 
-def cpu_baseline(args, layers, U, plans, outs, xs, cfg, wbytes_step, bytes_step):
-    """The fp64 oracle on the host cores, on a bounded sample of the same workload: the
-    step's forwards (one per token count) on layer 0, repeated while under the time budget.
-    Also checks the operator's outputs on those forwards against the oracle."""
+def cpu_info():
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count() or 1
+    return model, os.cpu_count() or 1, avail
+
+
+def cpu_baseline(args, w, TS):
+    """The fp64 oracle on the host cores, on a bounded sample of the headline workload: the
+    step's forwards (one per token count) on layer 0, timed on one core and with one token per
+    thread over all available cores (the oracle's tokens are independent; the C oracle runs
+    without the interpreter lock), each repeated while under the time budget.  Also checks the
+    operator's outputs on those forwards against the oracle."""
     import numpy as np
     import torch
+    from concurrent.futures import ThreadPoolExecutor
     from oracle import oracle
-    from paper_2609_04244_amd import monomoe as mm
     from paper_2609_04244_amd import workloads as wl
 
-    H, E, I, k, renorm = cfg["H"], cfg["E"], cfg["I"], cfg["k"], cfg["renorm"]
-    L = layers[0]
+    H, E, I, k, renorm = w.H, w.E, w.I, w.k, w.renorm
+    L = w.layers[0]
     rw = wl.bf16_bits(L["router_w"])
     bias = None if L["bias"] is None else L["bias"].cpu().numpy()
     sigmoid = L["policy"] == "sigmoid_bias"
     sel_bias = None if not sigmoid or L["sel_bias"] is None else L["sel_bias"].cpu().numpy()
     route = dict(policy=oracle.SIGMOID_BIAS, sel_bias=sel_bias, scale=L["route_scale"]) if sigmoid else {}
-    logits = oracle.router_logits(wl.bf16_bits(L["x"]), rw, bias)
-    if sigmoid:
-        ids, _ = oracle.select_sigmoid(logits, k, sel_bias, L["route_scale"])
-    else:
-        ids, _ = oracle.select(logits, k, renorm)
+    xb = {T: wl.bf16_bits(w.xs[(0, T)]) for T in TS}
+    logits = oracle.router_logits(xb[max(TS)], rw, bias)
+    ids = (oracle.select_sigmoid(logits, k, sel_bias, L["route_scale"])[0] if sigmoid
+           else oracle.select(logits, k, renorm)[0])
     ex = sorted(set(ids.reshape(-1).tolist()))
     idx = torch.tensor(ex, device=L["w13"].device)
     host = [t.index_select(0, idx).cpu().numpy() for t in (L["w13"], L["w13_scale"], L["w2"], L["w2_scale"])]
     tabs = [{e: a[i] for i, e in enumerate(ex)} for a in host]
-    worst = 0.0
-    mre_worst = 0.0
-    t0 = time.perf_counter()
-    reps = 0
-    while True:
-        for T in TS:
-            ref = oracle.forward(wl.bf16_bits(xs[(0, T)]), rw, *tabs, k, renorm, bias=bias, **route)
-            if reps == 0:
-                p = plans[T]
-                if L["bias"] is not None:
-                    p.set_router_bias(L["bias"])
-                if sigmoid:
-                    p.set_routing(mm.ROUTING_SIGMOID_BIAS, L["sel_bias"], L["route_scale"])
-                out = p.forward(xs[(0, T)], L["router_w"], L["w13"], L["w13_scale"], L["w2"], L["w2_scale"])
-                torch.cuda.synchronize()
-                got = out.float().cpu().numpy().astype(np.float64)
-                rms = float(np.sqrt(np.mean(ref ** 2)))
-                worst = max(worst, float(np.abs(got - ref).max()) / rms)
-                mre_worst = max(mre_worst, float(np.abs(got - ref).sum() / np.abs(ref).sum()))
-        reps += 1
-        if time.perf_counter() - t0 >= args.cpu_seconds:
-            break
-    dt = (time.perf_counter() - t0) / reps
-    u0 = sum(U[(0, T)] for T in TS)
-    wb0 = sum(U[(0, T)] * 3 * H * I for T in TS)
-    by0 = sum(algorithmic_bytes(U[(0, T)], T, H, E, I) for T in TS)
+
+    def one_token(T, t):
+        return oracle.forward(xb[T][t:t + 1], rw, *tabs, k, renorm, bias=bias, **route)
+
+    jobs = [(T, t) for T in TS for t in range(T)]
+    # GPU outputs of the sample's forwards, checked against the oracle once
+    worst = mre_worst = 0.0
+    refs = {}
+    for T, t in jobs:
+        refs[(T, t)] = one_token(T, t)
+    for T in TS:
+        w.route(T, L)
+        out = w.plans[T].forward(*w.args(0, T))
+        torch.cuda.synchronize()
+        got = out.float().cpu().numpy().astype(np.float64)
+        ref = np.concatenate([refs[(T, t)] for t in range(T)], axis=0)
+        rms = float(np.sqrt(np.mean(ref ** 2)))
+        worst = max(worst, float(np.abs(got - ref).max()) / rms)
+        mre_worst = max(mre_worst, float(np.abs(got - ref).sum() / np.abs(ref).sum()))
+
+    model, nproc, avail = cpu_info()
+    threads = max(1, min(avail, 16))
+
+    def timed(run):
+        reps = 0
+        t0 = time.perf_counter()
+        while True:
+            run()
+            reps += 1
+            if time.perf_counter() - t0 >= args.cpu_seconds:
+                break
+        return (time.perf_counter() - t0) / reps, reps
+
+    dt1, reps1 = timed(lambda: [one_token(T, t) for T, t in jobs])
+    with ThreadPoolExecutor(max_workers=threads) as pool:
+        dtn, repsn = timed(lambda: list(pool.map(lambda j: one_token(*j), jobs)))
+    by0 = sum(algorithmic_bytes(w.U[(0, T)], T, H, E, I) for T in TS)
     return {
-        "value": round(by0 / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-        "sample": "the step's %d forwards (T=%s) on layer 0, %d repetition(s), %.2f s each; "
-                  "%d selected experts in total" % (len(TS), ",".join(map(str, TS)), reps, dt, u0),
-        "ms_per_step": round(dt * 1e3, 1),
+        "value": round(by0 / dtn / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+        "sample": "the headline layer's step on weight set 0: %d forwards (T=%s, %d tokens, %d selected experts "
+                  "in total), one token per oracle call; %d repetition(s) on %d threads, %.3f s each; on one core "
+                  "%d repetition(s), %.3f s each" % (len(TS), ",".join(map(str, TS)), len(jobs),
+                                                      sum(w.U[(0, T)] for T in TS), repsn, threads, dtn, reps1, dt1),
+        "single_core": {"value": round(by0 / dt1 / 1e9, 4), "unit": "GB/s", "cores": 1,
+                        "ms_per_step": round(dt1 * 1e3, 1)},
+        "all_cores": {"value": round(by0 / dtn / 1e9, 4), "unit": "GB/s", "cores": threads,
+                      "ms_per_step": round(dtn * 1e3, 1)},
+        "cpu_model": model, "nproc": nproc, "cpus_available": avail,
         "gpu_vs_oracle_max_err_over_rms": round(worst, 5), "gpu_vs_oracle_mean_rel_err": round(mre_worst, 6),
     }
 
