@@ -207,6 +207,22 @@ __device__ __forceinline__ v4f block_mma(const v4i& a0, const v4i& a1, const v4i
     return c;
 }
 
+// The same 128-deep block contracted by one e4m3 x e4m3 MFMA (16x16x128, both operands
+// OCP E4M3, block scales 2^0) in the operand layout above: each lane's 32 bytes are its
+// eight dwords, in the same K order in A and B, so the products pair up as in block_mma.
+// Its block sums carry a relative error of about 2^-15 (measured), so it serves only the
+// down projection, whose block sums are scaled and accumulated but never requantised.
+typedef int v8i __attribute__((ext_vector_type(8)));
+constexpr int kMfmaFmtE4M3 = 0;
+constexpr int kMfmaScaleOne = 127;   // E8M0 exponent of 1.0
+__device__ __forceinline__ v4f block_mma_f8(const v4i& a0, const v4i& a1, const v4i& b0, const v4i& b1) {
+    const v8i a = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+    const v8i b = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
+    const v4f z = {0.f, 0.f, 0.f, 0.f};
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, z, kMfmaFmtE4M3, kMfmaFmtE4M3, 0, kMfmaScaleOne, 0,
+                                                            kMfmaScaleOne);
+}
+
 // Bounded wait until *p >= target on an LDS flag; false on abort or timeout.
 static __device__ bool wait_lds(const int* p, int target, const int* abort_flag, uint64_t limit) {
     if (lds_ld(p) >= target) {

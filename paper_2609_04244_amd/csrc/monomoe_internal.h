@@ -53,7 +53,8 @@ enum : int32_t { kRouteSoftmax = 0, kRouteSigmoidBias = 1 };
 constexpr int kStamps = 24;
 enum : int {
     kStEntry = 0, kStIssued, kStFirstData, kStMeta, kStUpComputed, kStUpDone, kStFirstAq, kStDownDone,
-    kStExit, kStFirstMfma, kStComputeDone, kStRouter, kStQuant, kStTopk, kStReduced, kStLogits, kStSelected, kStSeek, kStLbase,
+    kStExit, kStFirstMfma, kStComputeDone, kStRouter, kStQuant, kStTopk, kStReduced, kStLogits, kStSelected,
+    kStSeek, kStLbase, kStMask,
 };
 
 struct KParams {

@@ -360,6 +360,16 @@ class Plan:
         d["_keep"] = (ids_in, w_in)
         return out, d
 
+    def forward_stamped(self, x, router_w, w13, w13_scale, w2, w2_scale, out, stamps, stream=None):
+        """Forward with only the phase-stamp hook enabled: `stamps` is an int64 device tensor
+        [grid, 24] that receives each workgroup's s_memrealtime (100 MHz) stamps."""
+        dbg = Debug(None, None, None, None, None, None, None, None, None, None, stamps.data_ptr(), 0, 0)
+        rc = lib().monomoe_forward_debug(self._h, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale), _ptr(w2),
+                                         _ptr(w2_scale), _ptr(out), ctypes.byref(dbg), _stream(stream))
+        if rc != MONOMOE_OK:
+            raise MonoMoEError(rc, "monomoe_forward_debug")
+        return out
+
     def status(self):
         return lib().monomoe_plan_status(self._h)
 

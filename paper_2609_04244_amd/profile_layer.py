@@ -9,6 +9,8 @@ are generated here beforehand and saved as raw little-endian binaries:
   run:       the same launches from Python through the ctypes binding (no profiler needed);
   bench:     summarise a --kernel-trace --stats run of bench.py itself: the fused kernel's
              timed launches (the last --timed ones) against bench.py's own event timing;
+  timeline:  per-workgroup phase stamps of cold-cache launches (median and slowest
+             workgroup per phase) beside the dispatch-stamped launch time;
   summarize: turn the CSV output of one --kernel-trace run and two --pmc runs (FETCH_SIZE,
              WRITE_SIZE) of the C++ driver into a markdown summary and a JSON record: mean
              launch duration per token count, HBM bytes per launch from the counters scaled by
@@ -335,6 +337,111 @@ def bench_trace(args):
     print("\n".join(lines))
 
 
+# Phase stamps of the kernels (the kSt* indices of csrc/monomoe_internal.h), in the order
+# the phases happen; the label says which wavefront stamps it.
+STAMPS = [
+    (11, "router rows stored"),
+    (12, "input quantised (LDS)"),
+    (15, "all logits of token 0 seen (wave 0)"),
+    (16, "token 0 selected (wave 0)"),
+    (13, "top-k barrier passed"),
+    (19, "expert token masks built"),
+    (3, "routing metadata built"),
+    (17, "work partition found (wave 0)"),
+    (18, "first task addresses (wave 0)"),
+    (1, "weight ring filled (wave 0)"),
+    (2, "first weights used (wave 0)"),
+    (9, "first partial tile handed off (wave 0)"),
+    (4, "gate/up stream done (wave 0)"),
+    (5, "gate/up epilogues stored (helper)"),
+    (6, "first down activation requantised (helper)"),
+    (10, "down stream done (wave 0)"),
+    (7, "down epilogues stored (helper)"),
+    (14, "output chunks reduced"),
+    (8, "exit"),
+]
+
+
+def timeline(args):
+    """Per-workgroup phase stamps of cold-cache launches: for every phase, the median and
+    the slowest workgroup's time since the first workgroup started (medians over launches),
+    next to the dispatch-stamped launch time."""
+    import torch
+    from . import monomoe as mm
+    from . import workloads as wl
+    dev = torch.device("cuda:0")
+    Ts = [int(t) for t in args.T.split(",")]
+    cfg = wl.config(args.workload)
+    inp = wl.generate(cfg, T=max(Ts), seed=args.seed, device=dev)
+    flush_src = torch.empty(args.flush_mib << 20, dtype=torch.uint8, device=dev)
+    sink = torch.empty(16, dtype=torch.uint8, device=dev)
+    cols = {}
+    for T in Ts:
+        plan = mm.Plan(T, inp["H"], inp["E"], inp["I"], inp["k"], inp["renorm"])
+        if inp["bias"] is not None:
+            plan.set_router_bias(inp["bias"])
+        if inp["policy"] == "sigmoid_bias":
+            plan.set_routing(mm.ROUTING_SIGMOID_BIAS, inp["sel_bias"], inp["route_scale"])
+        G = plan.info()["grid"]
+        x = inp["x"][:T].contiguous()
+        out = torch.empty((T, inp["H"]), dtype=torch.bfloat16, device=dev)
+        w = (x, inp["router_w"], inp["w13"], inp["w13_scale"], inp["w2"], inp["w2_scale"])
+        stamps = torch.zeros((G, 24), dtype=torch.int64, device=dev)
+        per_phase = {i: ([], []) for i, _ in STAMPS}
+        launch_us, timed_us = [], []
+        timer = mm.DispatchTimer()
+        for it in range(args.warmup + args.iters):
+            mm.stream_read(flush_src, sink)            # evict the weights: a cold-cache launch
+            plan.forward_timed(*w, out, timer)
+            mm.stream_read(flush_src, sink)
+            stamps.zero_()
+            plan.forward_stamped(*w, out, stamps)
+            torch.cuda.synchronize()
+            if it < args.warmup:
+                continue
+            timed_us.append(timer.elapsed_ms() * 1e3)
+            s = stamps.cpu().numpy().astype(np.int64)
+            t0 = s[:, 0].min()
+            launch_us.append((s[:, 8].max() - t0) / 100.0)
+            for i, _ in STAMPS:
+                v = s[:, i]
+                v = v[v > 0]
+                if len(v):
+                    per_phase[i][0].append(float(np.median(v - t0)) / 100.0)
+                    per_phase[i][1].append(float(np.max(v - t0)) / 100.0)
+        if plan.status() != mm.MONOMOE_OK:
+            raise SystemExit("device status %s at T=%d" % (mm.status_string(plan.status()), T))
+        plan.close()
+        cols[T] = dict(launch=float(np.median(launch_us)), timed=float(np.median(timed_us)),
+                       phases={i: (float(np.median(a)), float(np.median(b))) if a else None
+                               for i, (a, b) in per_phase.items()})
+        print("T=%d: %d launches, stamped first entry to last exit %.2f us, untraced launch %.2f us"
+              % (T, args.iters, cols[T]["launch"], cols[T]["timed"]), flush=True)
+    lines = ["# Phase timeline: %s" % args.workload, ""]
+    if args.command:
+        lines += ["Command: `%s`" % args.command, ""]
+    lines += ["Per-workgroup phase stamps (s_memrealtime, 10 ns) of %d cold-cache launches per T (a %d MiB "
+              "streaming read before each), in us since the first workgroup started: median workgroup / "
+              "slowest workgroup, medians over the launches. Stamps come from the stamps-only debug forward; "
+              "the untraced launch time is the dispatch-stamped duration of the same launch without stamps."
+              % (args.iters, args.flush_mib), ""]
+    lines.append("| phase | " + " | ".join("T=%d" % T for T in Ts) + " |")
+    lines.append("|---|" + "---|" * len(Ts))
+    for i, label in STAMPS:
+        cells = []
+        for T in Ts:
+            v = cols[T]["phases"][i]
+            cells.append("—" if v is None else "%.2f / %.2f" % v)
+        lines.append("| %s | %s |" % (label, " | ".join(cells)))
+    lines.append("| first entry to last exit (stamped) | %s |" % " | ".join("%.2f" % cols[T]["launch"] for T in Ts))
+    lines.append("| untraced launch (dispatch-stamped events) | %s |" % " | ".join("%.2f" % cols[T]["timed"] for T in Ts))
+    text = "\n".join(lines) + "\n"
+    if args.out_md:
+        with open(args.out_md, "w") as fh:
+            fh.write(text)
+    print(text, flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -373,8 +480,19 @@ def main():
     bt.add_argument("--untraced-json", help="bench.py's output line from a run without the tracer")
     bt.add_argument("--command", default="")
     bt.add_argument("--out-md", required=True)
+    tl = sub.add_parser("timeline")
+    tl.add_argument("--workload", default="small_expert")
+    tl.add_argument("--T", default="1,8")
+    tl.add_argument("--iters", type=int, default=20)
+    tl.add_argument("--warmup", type=int, default=3)
+    tl.add_argument("--seed", type=int, default=0)
+    tl.add_argument("--flush-mib", type=int, default=1024)
+    tl.add_argument("--command", default="")
+    tl.add_argument("--out-md")
     args = ap.parse_args()
-    if args.cmd == "bench":
+    if args.cmd == "timeline":
+        timeline(args)
+    elif args.cmd == "bench":
         bench_trace(args)
     elif args.cmd == "generate":
         generate(args)
