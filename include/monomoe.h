@@ -247,10 +247,15 @@ int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info);
  *         MONOMOE_KERNEL_SINGLE (token passes of one tile each beyond it) or
  *         MONOMOE_KERNEL_MULTI (also below one tile);
  *   group_tokens: multi-tile only, a cap on R (0 = the largest the LDS holds), e.g. to
- *         study segment splitting.
+ *         study segment splitting;
+ *   general_only: single-tile only; 0 (default) runs passes of one token on the kernel's
+ *         one-token specialisation (the selected experts are the active ones, so each
+ *         workgroup starts streaming as soon as the experts it needs are ranked), 1 runs
+ *         them on the general kernel.
  * The task size and the per-expert workgroup groups follow from the weight-major partition
- * and are not separate parameters.  Schedules that differ only in grid or ring compute
- * bit-identical outputs; the kernel choice and R change the order of fp32 summation only.
+ * and are not separate parameters.  Schedules that differ only in grid, ring or
+ * general_only compute bit-identical outputs; the kernel choice and R change the order of
+ * fp32 summation only.
  * A new grid resets the plan's workspace (blocking; no launch of the plan may be pending).
  * Returns MONOMOE_ERR_INVALID (plan unchanged) for an out-of-range field, and
  * MONOMOE_ERR_UNSUPPORTED when the requested kernel cannot hold the shape's tiles. */
@@ -260,6 +265,7 @@ typedef struct {
     int32_t ring;
     int32_t kernel;
     int32_t group_tokens;
+    int32_t general_only;
 } monomoe_schedule_t;
 int monomoe_plan_set_schedule(monomoe_plan_t plan, const monomoe_schedule_t* sched);
 

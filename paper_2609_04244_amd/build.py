@@ -10,7 +10,8 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmonomoe.so")
-SOURCES = ["monomoe_kernel.hip", "monomoe_kernel_mt.hip", "monomoe_api.hip", "monomoe_stream.hip"]
+SOURCES = ["monomoe_kernel.hip", "monomoe_kernel_one.hip", "monomoe_kernel_mt.hip", "monomoe_api.hip",
+           "monomoe_stream.hip"]
 ARCH = "gfx950"
 
 

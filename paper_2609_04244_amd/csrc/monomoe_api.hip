@@ -46,6 +46,7 @@ struct monomoe_plan_s {
     int tchunk;   // tokens per pass (T larger than one LDS-resident tile runs in passes)
     int mt;       // multi-tile kernel
     int mt_rows, mt_pool, mt_tiles;
+    int general_only;           // schedule: no one-token specialisation
     KernelConfig cfg;           // the configuration above, as chosen for T
     KernelConfig small;         // single-tile configuration for forwards of at most small_T
     int small_T;                //   tokens when cfg is the multi-tile kernel (0: none)
@@ -106,15 +107,19 @@ int config_single(const monomoe_plan_s* pl, int ring, KernelConfig* c) {
     while (k.nslots < kSlotsMax && lds_dynamic_bytes(s.H, s.I, Tl, k.naq, k.nslots * 2) <= lds_cap) k.nslots *= 2;
     k.lds_dyn = lds_dynamic_bytes(s.H, s.I, Tl, k.naq, k.nslots);
     if (k.lds_dyn > lds_cap) return MONOMOE_ERR_UNSUPPORTED;
+    k.occupancy = 0;
     for (const KernelVariant& v : pl->kern->v) {
-        hipFuncAttributes va;
-        int o = 0;
-        if (hipFuncGetAttributes(&va, v.fn) != hipSuccess || allow_full_lds(v.fn, pl->lds_total, &va) != hipSuccess ||
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, v.fn, kThreads, (size_t)k.lds_dyn) != hipSuccess)
-            return MONOMOE_ERR_HIP;
-        if ((int)va.sharedSizeBytes + k.lds_dyn > pl->lds_total) return MONOMOE_ERR_UNSUPPORTED;
-        if (o < 1) return MONOMOE_ERR_OCCUPANCY;
-        if (&v == var) k.occupancy = o;
+        for (const void* fn : {v.fn, v.fn1}) {   // the kernel and its one-token specialisation
+            if (!fn) continue;
+            hipFuncAttributes va;
+            int o = 0;
+            if (hipFuncGetAttributes(&va, fn) != hipSuccess || allow_full_lds(fn, pl->lds_total, &va) != hipSuccess ||
+                hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, fn, kThreads, (size_t)k.lds_dyn) != hipSuccess)
+                return MONOMOE_ERR_HIP;
+            if ((int)va.sharedSizeBytes + k.lds_dyn > pl->lds_total) return MONOMOE_ERR_UNSUPPORTED;
+            if (o < 1) return MONOMOE_ERR_OCCUPANCY;
+            if (&v == var) k.occupancy = k.occupancy ? std::min(k.occupancy, o) : o;
+        }
     }
     *c = k;
     return MONOMOE_OK;
@@ -229,9 +234,13 @@ int configure_plan(monomoe_plan_s* pl, int dev, int num_cus, int lds_total) {
     const int cr = configure(pl, MONOMOE_KERNEL_AUTO, 0, 0, &cfg, &small, &small_T);
     if (cr != MONOMOE_OK) return cr;
     apply_config(pl, cfg, small, small_T);
-    hipFuncAttributes attr;
-    if (hipFuncGetAttributes(&attr, pl->var->fn) != hipSuccess) return MONOMOE_ERR_HIP;
-    pl->private_bytes = (int)attr.localSizeBytes;
+    pl->private_bytes = 0;
+    for (const void* fn : {pl->var->fn, pl->var->fn1}) {
+        hipFuncAttributes attr;
+        if (!fn) continue;
+        if (hipFuncGetAttributes(&attr, fn) != hipSuccess) return MONOMOE_ERR_HIP;
+        pl->private_bytes = std::max(pl->private_bytes, (int)attr.localSizeBytes);
+    }
     pl->grid = pl->num_cus;   // one resident workgroup per CU
     if (pl->grid > kGridMax) return MONOMOE_ERR_UNSUPPORTED;
     return MONOMOE_OK;
@@ -356,15 +365,18 @@ int launch(monomoe_plan_t plan, int T, const void* x, const void* router_w, cons
         if (p.inj_ids) q.inj_ids = p.inj_ids + (size_t)t0 * K;
         if (p.inj_w) q.inj_w = p.inj_w + (size_t)t0 * K;
         const bool first = t0 == 0, last = t0 + tc >= T;
+        // a pass of one token runs the one-token specialisation (not under the timeout test hook)
+        const bool one = q.T == 1 && !q.fail_flag && cf.var->fn1 != nullptr && !plan->general_only;
         if (ev_start || ev_stop) {
             // the dispatch itself records the events (the first pass's begin, the last
             // pass's end), not the stream
             void* args[] = {&q};
-            if (hipExtLaunchKernel(cf.var->fn, dim3(plan->grid), dim3(kThreads), args, (size_t)cf.lds_dyn,
-                                   stream, first ? ev_start : nullptr, last ? ev_stop : nullptr, 0) != hipSuccess)
+            if (hipExtLaunchKernel(one ? cf.var->fn1 : cf.var->fn, dim3(plan->grid), dim3(kThreads), args,
+                                   (size_t)cf.lds_dyn, stream, first ? ev_start : nullptr, last ? ev_stop : nullptr,
+                                   0) != hipSuccess)
                 return MONOMOE_ERR_HIP;
         } else {
-            cf.var->launch(q, plan->grid, (size_t)cf.lds_dyn, stream);
+            (one ? cf.var->launch1 : cf.var->launch)(q, plan->grid, (size_t)cf.lds_dyn, stream);
         }
         if (hipGetLastError() != hipSuccess) return MONOMOE_ERR_HIP;
     }
@@ -580,6 +592,7 @@ int monomoe_plan_set_schedule(monomoe_plan_t plan, const monomoe_schedule_t* sch
     if (sched->kernel < MONOMOE_KERNEL_AUTO || sched->kernel > MONOMOE_KERNEL_MULTI) return MONOMOE_ERR_INVALID;
     if (sched->group_tokens < 0 || sched->group_tokens > kTLimit) return MONOMOE_ERR_INVALID;
     if (sched->ring != 0 && sched->ring != kRings[0] && sched->ring != kRings[1]) return MONOMOE_ERR_INVALID;
+    if (sched->general_only != 0 && sched->general_only != 1) return MONOMOE_ERR_INVALID;
     int dev = -1;
     if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return MONOMOE_ERR_INVALID;
     KernelConfig cfg{}, small{};
@@ -596,6 +609,7 @@ int monomoe_plan_set_schedule(monomoe_plan_t plan, const monomoe_schedule_t* sch
         if (zr != MONOMOE_OK) return zr;
     }
     plan->grid = grid;
+    plan->general_only = sched->general_only;
     apply_config(plan, cfg, small, small_T);
     return MONOMOE_OK;
 }
@@ -652,6 +666,9 @@ int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info) {
     info->workspace_bytes = (int64_t)plan->ws_bytes;
     hipFuncAttributes attr;
     info->scratch_bytes = hipFuncGetAttributes(&attr, plan->var->fn) == hipSuccess ? (int32_t)attr.localSizeBytes : -1;
+    if (plan->var->fn1 && info->scratch_bytes >= 0)   // and its one-token specialisation
+        info->scratch_bytes = hipFuncGetAttributes(&attr, plan->var->fn1) == hipSuccess
+                                  ? std::max(info->scratch_bytes, (int32_t)attr.localSizeBytes) : -1;
     info->ring = plan->var->ring;
     info->tokens_per_pass = plan->tchunk;
     info->multi_tile = plan->mt;

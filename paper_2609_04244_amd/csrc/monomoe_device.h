@@ -257,11 +257,12 @@ __device__ __forceinline__ float row16_max(float x) {
 // then the fp32 scales [T,H/128]).  Sixteen lanes (one DPP row) own one 128-element
 // group, eight values each: s = amax/448 and codes = e4m3(v/s) with the fp32 quotient
 // (quot_rn), the same arithmetic as every other quantisation in this file.  Scale rows
-// T..kTMax-1 are zeroed.  All threads of the workgroup take part.
-template <int H>
+// T..kTMax-1 are zeroed.  Threads 0 .. NTH-1 take part (all of the workgroup by default).
+template <int H, int NTH = kThreads>
 __device__ __forceinline__ void quantise_input(const uint16_t* __restrict__ x, int T, uint8_t* xq_s, float* xs_s,
                                                int tid, uint8_t* d_xq, float* d_xs) {
     constexpr int HB = H / 128, XROW = H + 16, CPR = H / 8, UNR = 4;
+    constexpr int kThreads = NTH;   // the threads taking part: tid in [0, NTH)
     const int nch = T * CPR;   // a multiple of 16, so DPP rows are all valid or all not
     for (int c0 = 0; c0 < nch; c0 += UNR * kThreads) {
         // All loads of a pass are issued back to back (clamped addresses, no branches in
@@ -461,12 +462,14 @@ __device__ __forceinline__ int wave_max_i32(int x) {
 // nullptr skips token n); an expert that cannot be determined (NaN logits) is reported
 // as -1.  The routing weights are computed later, by routing_weights.  The logits are tagged words: the wavefront polls until
 // every word carries this launch's tag (false on timeout or when another workgroup has
-// recorded an error).
+// recorded an error).  With `publish` (an LDS counter; one token), each round's selection is
+// also written to ids[0][j] at once and the counter raised to j + 1, so consumers of the
+// first selections need not wait for the last.
 template <int EPL, int NT>
 __device__ __forceinline__ bool topk_tokens(const uint64_t* const* rows, int E, int K, int lane,
                                             uint32_t tag, uint32_t* status, uint64_t limit, int* const* ids,
                                             int policy, const float* sel_bias, uint64_t* st_logits,
-                                            uint64_t* st_selected) {
+                                            uint64_t* st_selected, int* publish = nullptr) {
     float lv[NT][EPL];
     float bias[EPL];   // expert-selection bias of sigmoid routing
 #pragma unroll
@@ -540,6 +543,10 @@ __device__ __forceinline__ bool topk_tokens(const uint64_t* const* rows, int E, 
             if (lane == j) {
                 my_key[n] = bk;
                 my_id[n] = bi;
+            }
+            if (publish != nullptr && n == 0 && lane == 0) {   // this round's selection, at once
+                ids[0][j] = bi;
+                lds_st(publish, j + 1);
             }
         }
     }
@@ -629,11 +636,12 @@ __device__ __forceinline__ void routing_weights(const uint64_t* logits, const in
 template <int NT>
 __device__ __forceinline__ bool topk_bucket(const uint64_t* const* rows, int E, int K, int lane, uint32_t tag,
                                             uint32_t* status, uint64_t limit, int* const* ids, int policy,
-                                            const float* sel_bias, uint64_t* stl, uint64_t* sts) {
-    if (E <= 64) return topk_tokens<1, NT>(rows, E, K, lane, tag, status, limit, ids, policy, sel_bias, stl, sts);
-    if (E <= 128) return topk_tokens<2, NT>(rows, E, K, lane, tag, status, limit, ids, policy, sel_bias, stl, sts);
-    if (E <= 256) return topk_tokens<4, NT>(rows, E, K, lane, tag, status, limit, ids, policy, sel_bias, stl, sts);
-    return topk_tokens<8, NT>(rows, E, K, lane, tag, status, limit, ids, policy, sel_bias, stl, sts);
+                                            const float* sel_bias, uint64_t* stl, uint64_t* sts,
+                                            int* publish = nullptr) {
+    if (E <= 64) return topk_tokens<1, NT>(rows, E, K, lane, tag, status, limit, ids, policy, sel_bias, stl, sts, publish);
+    if (E <= 128) return topk_tokens<2, NT>(rows, E, K, lane, tag, status, limit, ids, policy, sel_bias, stl, sts, publish);
+    if (E <= 256) return topk_tokens<4, NT>(rows, E, K, lane, tag, status, limit, ids, policy, sel_bias, stl, sts, publish);
+    return topk_tokens<8, NT>(rows, E, K, lane, tag, status, limit, ids, policy, sel_bias, stl, sts, publish);
 }
 
 // Router logits of experts wg, wg + G, ... (Sec. 4.1): the bf16 dot product of each

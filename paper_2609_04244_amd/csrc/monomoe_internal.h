@@ -109,6 +109,9 @@ struct KernelVariant {
     int ring;
     const void* fn;                                          // __global__ symbol
     void (*launch)(const KParams&, int grid, size_t lds, hipStream_t);
+    // the same kernel specialised for one token (T = 1; null: none), with the same LDS layout
+    const void* fn1;
+    void (*launch1)(const KParams&, int grid, size_t lds, hipStream_t);
 };
 struct KernelEntry {
     int H, I;

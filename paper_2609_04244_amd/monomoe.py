@@ -62,7 +62,7 @@ class PlanInfo(ctypes.Structure):
 
 class Schedule(ctypes.Structure):
     _fields_ = [("grid", ctypes.c_int32), ("ring", ctypes.c_int32), ("kernel", ctypes.c_int32),
-                ("group_tokens", ctypes.c_int32)]
+                ("group_tokens", ctypes.c_int32), ("general_only", ctypes.c_int32)]
 
 
 _lib = None
@@ -255,10 +255,12 @@ class Plan:
             raise MonoMoEError(rc, "monomoe_plan_set_routing")
         self._sel_bias = sel_bias  # keep the tensor alive while the plan refers to it
 
-    def set_schedule(self, grid=0, ring=0, kernel=KERNEL_AUTO, group_tokens=0):
+    def set_schedule(self, grid=0, ring=0, kernel=KERNEL_AUTO, group_tokens=0, general_only=0):
         """Persistent grid (0 = one workgroup per CU), weight-ring depth (0 = default), kernel
-        (KERNEL_AUTO / KERNEL_SINGLE / KERNEL_MULTI) and the multi-tile segment cap (0 = none)."""
-        sch = Schedule(int(grid), int(ring), int(kernel), int(group_tokens))
+        (KERNEL_AUTO / KERNEL_SINGLE / KERNEL_MULTI), the multi-tile segment cap (0 = none), and
+        general_only (1: passes of one token on the general single-tile kernel, not its
+        one-token specialisation)."""
+        sch = Schedule(int(grid), int(ring), int(kernel), int(group_tokens), int(general_only))
         rc = lib().monomoe_plan_set_schedule(self._h, ctypes.byref(sch))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_plan_set_schedule")
