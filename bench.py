@@ -1,9 +1,10 @@
 #!/usr/bin/env python3
 """Benchmark of the fused routed-MoE decode operator on one MI355X.
 
-One step = one forward of the operator for each decode token count T in {1, 2, 4, 8}; each of
-the evaluated layers is timed in its own block of steps (the paper's isolated-operator
-protocol, consecutive launches of one operator):
+One step = one forward of the operator for each decode token count T in {1, 2, 4, 8}; each
+(layer, T) is timed over its own block of consecutive launches (the paper's isolated-operator
+protocol, repeated launches of one operator configuration, as the MoE layers of one decode step
+at one batch size run; `--order interleaved` cycles T within every step instead).  The layers:
   wide_fine         H=7168 E=256 I=2048 top-8, renormalised softmax (the headline: the largest
                     evaluated layer that fits one GPU, ~11 GB of FP8 expert weights),
   small_expert      H=2048 E=128 I=768  top-8, renormalised softmax,
@@ -15,9 +16,10 @@ so every launch streams its weights from HBM, as consecutive MoE layers of a dec
 
 Each launch's duration comes from HIP events that its own dispatch stamps (hipExtLaunchKernel
 through monomoe_forward_timed): the kernel's begin and end, as a kernel trace reports them.
-Each (layer, T) forward is also captured into a HIP graph and its replays are event-timed on
-the stream (the paper's protocol: graph replays after warm-ups), reported beside the kernel
-time.
+The forwards of every weight set at one T are also captured into one HIP graph (as a decode
+step's graph holds a model's MoE layers) and its replays are event-timed on the stream (the
+paper's protocol: graph replays after warm-ups); replay time over the graph's launches is
+reported beside the kernel time.
 
 Printed (one JSON line): value = algorithmic bytes / summed launch time (GB/s) of the headline
 layer over its token counts; per-T latency (mean, p10/p50/p90, graph replay p50), achieved GB/s
@@ -66,8 +68,12 @@ def parse():
     ap.add_argument("--tokens", default="1,2,4,8",
                     help="decode token counts of one step (up to 64; the metric is quoted on 1,2,4,8)")
     ap.add_argument("--layers", type=int, default=0, help="weight sets per workload (0: as the reuse bound needs)")
-    ap.add_argument("--replays", type=int, default=100, help="timed graph replays per (layer, T); 0: none")
+    ap.add_argument("--replays", type=int, default=100,
+                    help="timed launches per T in graph replays (a replay launches every weight set once); 0: none")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--order", choices=("blocked", "interleaved"), default="blocked",
+                    help="blocked: each (layer, T) timed over consecutive launches; interleaved: T cycles "
+                         "within every step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="per oracle mode (one core, all cores)")
     return ap.parse_args()
@@ -173,34 +179,37 @@ class Workload:
         self.records[T].append((l, timer, timed))
 
     def capture_graphs(self):
-        """One HIP graph per (layer, T), each replaying that layer's forward."""
+        """One HIP graph per T holding a forward of every weight set in turn (as a decode step's
+        graph holds the MoE layers of a model), so a replay is n consecutive operator launches."""
         import torch
         self.graphs = {}
         side = torch.cuda.Stream()
         for T in self.TS:
             for l in range(self.n):
-                self.route(T, self.layers[l])   # the routing inputs are read from the plan at capture
+                self.route(T, self.layers[l])
                 side.wait_stream(torch.cuda.current_stream())
                 with torch.cuda.stream(side):
                     self.plans[T].forward(*self.args(l, T), out=self.outs[T])
                 torch.cuda.current_stream().wait_stream(side)
-                g = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(g):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for l in range(self.n):
+                    self.route(T, self.layers[l])   # the routing inputs are read from the plan at capture
                     self.plans[T].forward(*self.args(l, T), out=self.outs[T], check=False)
-                self.graphs[(l, T)] = g
+            self.graphs[T] = g
         torch.cuda.synchronize()
 
     def replay(self, T, timed):
+        """One replay of T's graph; with `timed`, events around it (the replay time over the
+        graph's n launches is the per-launch figure)."""
         import torch
-        l = self.next_layer
-        self.next_layer = (l + 1) % self.n
         if not timed:
-            self.graphs[(l, T)].replay()
+            self.graphs[T].replay()
             return None
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
         a.record()
-        self.graphs[(l, T)].replay()
+        self.graphs[T].replay()
         b.record()
         return (a, b)
 
@@ -290,27 +299,33 @@ def main():
         w.select()
 
     # dispatch-stamped kernel times, one layer after the other (the paper's isolated-operator
-    # protocol: consecutive launches of one operator shape); a step is one launch per T
+    # protocol: consecutive launches of one operator configuration).  Blocked order (default):
+    # each (layer, T) runs warmup + steps consecutive launches, as the MoE layers of a decode
+    # step at one batch size do; interleaved order: every step launches T = 1, 2, 4, 8 in turn.
+    # A step is one launch per T either way.
     stream = torch.cuda.current_stream()
     wall = 0.0
     ms_per_step = 0.0
+    blocks = [[T] for T in TS] if args.order == "blocked" else [list(TS)]
     for w in wls:
-        torch.cuda.synchronize()
-        w_start = torch.cuda.Event(enable_timing=True)
-        w_end = torch.cuda.Event(enable_timing=True)
-        t_start = None
-        for s in range(args.warmup + args.steps):
-            if s == args.warmup:
-                torch.cuda.synchronize()
-                t_start = time.perf_counter()
-                w_start.record(stream)
-            for T in TS:
-                w.launch(T, s >= args.warmup)
-        w_end.record(stream)
-        torch.cuda.synchronize()
-        wall += time.perf_counter() - t_start
+        w.ms_per_step = 0.0
+        for blk in blocks:
+            torch.cuda.synchronize()
+            w_start = torch.cuda.Event(enable_timing=True)
+            w_end = torch.cuda.Event(enable_timing=True)
+            t_start = None
+            for s in range(args.warmup + args.steps):
+                if s == args.warmup:
+                    torch.cuda.synchronize()
+                    t_start = time.perf_counter()
+                    w_start.record(stream)
+                for T in blk:
+                    w.launch(T, s >= args.warmup)
+            w_end.record(stream)
+            torch.cuda.synchronize()
+            wall += time.perf_counter() - t_start
+            w.ms_per_step += w_start.elapsed_time(w_end) / args.steps
         w.status_ok()
-        w.ms_per_step = w_start.elapsed_time(w_end) / args.steps
         ms_per_step += w.ms_per_step
 
     # graph replays, event-timed on the stream, same order and layer rotation
@@ -318,14 +333,16 @@ def main():
         for w in wls:
             w.capture_graphs()
             pending = []
-            for r in range(20 + args.replays):
-                for T in TS:
-                    ev = w.replay(T, r >= 20)
-                    if ev is not None:
-                        pending.append((T, ev))
+            reps = max(1, args.replays // w.n)   # graph replays of n launches each
+            for blk in blocks:
+                for r in range(5 + reps):
+                    for T in blk:
+                        ev = w.replay(T, r >= 5)
+                        if ev is not None:
+                            pending.append((T, ev))
             torch.cuda.synchronize()
             for T, (a, b) in pending:
-                w.graph_ms[T].append(a.elapsed_time(b))
+                w.graph_ms[T].append(a.elapsed_time(b) / w.n)
             w.status_ok()
 
     blocks = {}
@@ -347,8 +364,9 @@ def main():
             "other_workloads": [b["layer"] for n, b in blocks.items() if n != w0.name],
             "launches_per_step": len(TS) * len(wls), "grid": w0.plans[TS[0]].info()["grid"],
             "block": w0.plans[TS[0]].info()["block"],
-            "step": "one forward per token count; each layer is timed in its own block of steps; value, per_T and "
-                    "roofline are the headline layer's; ms_per_step sums one step of every layer",
+            "step": "one forward per token count; each (layer, T) is timed over its own block of consecutive "
+                    "launches (order %s); value, per_T and roofline are the headline layer's; ms_per_step sums "
+                    "one launch of every T of every layer" % args.order,
         },
         "per_T": blk0["per_T"],
         "workloads": blocks,
