@@ -2,29 +2,38 @@
 precompiled for a set of schedules; candidates that fail numerical validation are
 rejected and the rest ranked by latency over the target token-count range).
 
-A schedule here is (kernel, grid, ring): the single-tile or multi-tile kernel, the
-persistent workgroup count and the weight-ring depth (see monomoe_plan_set_schedule).  For
-one workload and a list of token counts:
+A schedule here is (kernel, grid, ring, one-token specialisation, segment cap): the
+single-tile or multi-tile kernel, the persistent workgroup count, the weight-ring depth,
+whether passes of one token run on the single-tile kernel's one-token specialisation, and
+the multi-tile kernel's cap on tokens per expert segment (see monomoe_plan_set_schedule).
+For one workload and a list of token counts:
 
-  1. enumerate kernel x grid x ring candidates (combinations the plan rejects are dropped:
-     the multi-tile kernel has ring depth 2 only, grids must be resident);
+  1. enumerate the candidates (combinations the plan rejects are dropped: the multi-tile
+     kernel has ring depth 2 only, grids must be resident);
   2. validation gate, against the default schedule's output on the same inputs (the default
-     is what the parity tests check against the fp64 oracle), with the device status OK: a
-     candidate that runs the same kernel must be bit-identical (grid and ring change when and
-     where the work runs, never the arithmetic); one that runs the other kernel sums in
-     another order and must be within the operator's output bound (max |diff| <= 2e-2 rms,
-     mean relative difference <= 5e-3);
-  3. rank the survivors by the sum over the token counts of the mean dispatch-stamped
-     launch time, with layers rotated so every launch streams its weights from HBM.
+     is what the parity tests check against the fp64 oracle; the package itself does not use
+     the oracle, and tests/test_gpu_tuned_schedules.py runs every tuned schedule against it),
+     with the device status OK: a candidate that runs the same kernel must be bit-identical
+     (grid, ring and the one-token specialisation change when and where the work runs, never
+     the arithmetic); one that runs the other kernel or caps the segments sums in another
+     order and must be within the operator's output bound (max |diff| <= 2e-2 rms, mean
+     relative difference <= 5e-3);
+  3. rank the survivors by the sum over the token counts of the per-launch time of HIP graph
+     replays (one graph per T holding a forward of every rotated layer, so every launch
+     streams its weights from HBM), the dispatch-stamped launch time reported beside it.
 
-Writes a markdown summary (the command, every candidate's per-T latency, the ranking).
+Writes a markdown summary (the command, every candidate's per-T latency, the ranking) and,
+with --table, records the best schedule per T in a JSON table (tuned_schedules.json next to
+this file: {workload: {T: schedule}}), which `apply_tuned` reads.
 
 Example:
   python3 -m paper_2609_04244_amd.tune --workload small_expert --T 1,2,4,8 \\
-      --grids 0,192,128 --rings 2,4 --kernels single,multi \\
+      --grids 0,192 --rings 2,4 --kernels single,multi --table \\
       --out profiles/schedule_tuning_small_expert.md
 """
 import argparse
+import json
+import os
 import sys
 
 import numpy as np
@@ -34,21 +43,64 @@ from . import monomoe as mm
 from . import workloads as wl
 
 
+TABLE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "tuned_schedules.json")
+
+
 def run(plan, L, T, out):
     return plan.forward(L["x"][:T].contiguous(), L["router_w"], L["w13"], L["w13_scale"], L["w2"], L["w2_scale"],
                         out=out, check=False)
+
+
+def load_table(path=TABLE):
+    """The tuned schedules, {workload: {T: schedule}} ({} when there is no table)."""
+    if not os.path.exists(path):
+        return {}
+    with open(path) as fh:
+        return json.load(fh)
+
+
+def tuned_schedule(workload, T, path=TABLE):
+    """The tuned schedule of `workload` at T tokens (a dict of set_schedule's keyword
+    arguments), or None when the table has none."""
+    e = load_table(path).get(workload, {}).get(str(T))
+    return None if e is None else {k: e[k] for k in SCHEDULE_KEYS}
+
+
+def apply_tuned(plan, workload, T, path=TABLE):
+    """Set the tuned schedule of `workload` at T on `plan`; False (plan unchanged) if none."""
+    sch = tuned_schedule(workload, T, path)
+    if sch is None:
+        return False
+    plan.set_schedule(**sch)
+    return True
+
+
+SCHEDULE_KEYS = ("kernel", "grid", "ring", "general_only", "group_tokens")
+TIE = 0.01   # a schedule replaces the default at T only when faster by more than this fraction
+KERNEL_NAMES = {mm.KERNEL_SINGLE: "single", mm.KERNEL_MULTI: "multi"}
+
+
+def label(c):
+    s = "%s/%d/%d" % (KERNEL_NAMES[c[0]], c[1], c[2])
+    if c[0] == mm.KERNEL_SINGLE and c[3]:
+        s += " general"
+    if c[0] == mm.KERNEL_MULTI and c[4]:
+        s += " R<=%d" % c[4]
+    return s
 
 
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--workload", default="small_expert")
     ap.add_argument("--T", default="1,2,4,8")
-    ap.add_argument("--grids", default="0,192,128", help="persistent grids (0 = one workgroup per CU)")
+    ap.add_argument("--grids", default="0,192", help="persistent grids (0 = one workgroup per CU)")
     ap.add_argument("--rings", default="2,4")
     ap.add_argument("--kernels", default="single", help="single, multi or both (comma-separated)")
+    ap.add_argument("--group-tokens", default="0", help="multi-tile segment caps (0 = none), comma-separated")
     ap.add_argument("--layers", type=int, default=8)
-    ap.add_argument("--iters", type=int, default=48)
+    ap.add_argument("--replays", type=int, default=6, help="timed graph replays (of --layers launches each)")
     ap.add_argument("--reps", type=int, default=2)
+    ap.add_argument("--table", action="store_true", help="record the best schedule per T in tuned_schedules.json")
     ap.add_argument("--out", default=None)
     ap.add_argument("--command", default=None, help="command text recorded in the summary")
     args = ap.parse_args(argv)
@@ -60,31 +112,47 @@ def main(argv=None):
 
     def make_plan(T, L):
         plan = mm.Plan(T, cfg["H"], cfg["E"], cfg["I"], cfg["k"], cfg["renorm"])
+        route(plan, L)
+        return plan
+
+    def route(plan, L):
         if L["bias"] is not None:
             plan.set_router_bias(L["bias"])
         if L["policy"] == "sigmoid_bias":
             plan.set_routing(mm.ROUTING_SIGMOID_BIAS, L["sel_bias"], L["route_scale"])
-        return plan
+
+    def schedule(plan, c):
+        plan.set_schedule(kernel=c[0], grid=c[1], ring=c[2], general_only=c[3], group_tokens=c[4])
 
     kmode = {"single": mm.KERNEL_SINGLE, "multi": mm.KERNEL_MULTI}
     probe = make_plan(Ts[0], layers[0])
     info = probe.info()
     probe.close()
+    # candidate: (kernel, grid, ring, general_only, group_tokens)
     cands = []
     for kn in args.kernels.split(","):
         for g in (int(x) for x in args.grids.split(",")):
-            for r in (int(x) for x in args.rings.split(",")):
-                if kn == "multi" and r != 2:
-                    continue   # the multi-tile kernel has ring depth 2 only
-                cands.append((kn, g if g else info["num_cus"], r))
+            g = g if g else info["num_cus"]
+            if kn == "multi":   # ring depth 2 only; segment caps
+                for R in (int(x) for x in args.group_tokens.split(",")):
+                    cands.append((mm.KERNEL_MULTI, g, 2, 0, R))
+            else:
+                for r in (int(x) for x in args.rings.split(",")):
+                    for gen in ((0, 1) if 1 in Ts else (0,)):   # the specialisation matters at T = 1 only
+                        cands.append((mm.KERNEL_SINGLE, g, r, gen, 0))
 
     # 1-2. enumeration and validation gate
-    valid, rejected, defaults = [], {}, {}
+    rejected, defaults, one_pass = {}, {}, {}
     for T in Ts:
         plan = make_plan(T, layers[0])
+        plan.set_schedule(kernel=mm.KERNEL_SINGLE)
+        tpp = plan.info()["tokens_per_pass"]
+        one_pass[T] = (T - 1) % tpp == 0   # the single-tile kernel's last pass has one token
+        plan.close()
+        plan = make_plan(T, layers[0])
         dinfo = plan.info()
-        dk = "multi" if dinfo["multi_tile"] else "single"
-        defaults[T] = (dk, dinfo["grid"], dinfo["ring"])
+        dk = mm.KERNEL_MULTI if dinfo["multi_tile"] else mm.KERNEL_SINGLE
+        defaults[T] = (dk, dinfo["grid"], dinfo["ring"], 0, 0)
         out = torch.empty((T, cfg["H"]), dtype=torch.bfloat16, device=dev)
         ref = run(plan, layers[0], T, out).clone()
         reff = ref.float()
@@ -93,7 +161,7 @@ def main(argv=None):
             if c in rejected:
                 continue
             try:
-                plan.set_schedule(kernel=kmode[c[0]], grid=c[1], ring=c[2])
+                schedule(plan, c)
             except mm.MonoMoEError as e:
                 rejected[c] = "not accepted: %s" % e
                 continue
@@ -102,7 +170,7 @@ def main(argv=None):
             if plan.status() != mm.MONOMOE_OK:
                 rejected[c] = "device status %s at T=%d" % (mm.status_string(plan.status()), T)
                 plan.reset()
-            elif c[0] == dk:
+            elif c[0] == dk and c[4] == 0:
                 if not torch.equal(o.view(torch.int16), ref.view(torch.int16)):
                     rejected[c] = "output differs from the default schedule at T=%d" % T
             else:
@@ -110,60 +178,120 @@ def main(argv=None):
                 if float(d.max()) > 2e-2 * rms or float(d.sum() / reff.abs().sum()) > 5e-3:
                     rejected[c] = "output outside the bound of the default schedule's at T=%d" % T
         plan.close()
+        print("validated T=%d" % T, flush=True)
     valid = [c for c in cands if c not in rejected]
     print("candidates %d, valid %d" % (len(cands), len(valid)), flush=True)
 
-    # 3. ranking by latency over the token-count range
-    lat = {}
+    # 3. ranking by graph-replay latency over the token-count range (dispatch-stamped too)
+    lat, dsp = {}, {}
+    n = len(layers)
     for rep in range(args.reps):
         for T in Ts:
             plan = make_plan(T, layers[0])
             out = torch.empty((T, cfg["H"]), dtype=torch.bfloat16, device=dev)
             xs = [L["x"][:T].contiguous() for L in layers]
+            side = torch.cuda.Stream()
             for c in valid:
-                plan.set_schedule(kernel=kmode[c[0]], grid=c[1], ring=c[2])
-                for i in range(len(layers)):   # warm-up
+                if c[3] and not one_pass[T]:
+                    continue   # without a one-token pass the specialisation is not used: the same schedule
+                schedule(plan, c)
+                for i in range(n):   # warm-up (also before capture, on a side stream)
                     L = layers[i]
-                    plan.forward(xs[i], L["router_w"], L["w13"], L["w13_scale"], L["w2"], L["w2_scale"], out=out,
-                                 check=False)
-                timers = [mm.DispatchTimer() for _ in range(args.iters)]
-                for i in range(args.iters):
-                    L = layers[i % len(layers)]
-                    plan.forward_timed(xs[i % len(layers)], L["router_w"], L["w13"], L["w13_scale"], L["w2"],
-                                       L["w2_scale"], out, timers[i])
+                    route(plan, L)
+                    side.wait_stream(torch.cuda.current_stream())
+                    with torch.cuda.stream(side):
+                        plan.forward(xs[i], L["router_w"], L["w13"], L["w13_scale"], L["w2"], L["w2_scale"],
+                                     out=out, check=False)
+                    torch.cuda.current_stream().wait_stream(side)
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g):
+                    for i in range(n):
+                        L = layers[i]
+                        route(plan, L)
+                        plan.forward(xs[i], L["router_w"], L["w13"], L["w13_scale"], L["w2"], L["w2_scale"],
+                                     out=out, check=False)
+                g.replay()
+                evs = []
+                for r in range(args.replays):
+                    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    a.record()
+                    g.replay()
+                    b.record()
+                    evs.append((a, b))
+                timers = [mm.DispatchTimer() for _ in range(n)]
+                for i in range(n):
+                    L = layers[i]
+                    route(plan, L)
+                    plan.forward_timed(xs[i], L["router_w"], L["w13"], L["w13_scale"], L["w2"], L["w2_scale"], out,
+                                       timers[i])
                 torch.cuda.synchronize()
-                assert plan.status() == mm.MONOMOE_OK
-                us = float(np.mean([t.elapsed_ms() * 1e3 for t in timers]))
-                lat.setdefault((c, T), []).append(us)
+                assert plan.status() == mm.MONOMOE_OK, label(c)
+                lat.setdefault((c, T), []).append(float(np.median([a.elapsed_time(b) for a, b in evs])) * 1e3 / n)
+                dsp.setdefault((c, T), []).append(float(np.mean([t.elapsed_ms() for t in timers])) * 1e3)
+                del g
             plan.close()
+            print("ranked T=%d (repetition %d of %d)" % (T, rep + 1, args.reps), flush=True)
     best_us = {k: min(v) for k, v in lat.items()}
+    best_dsp = {k: min(v) for k, v in dsp.items()}
+    for c in valid:   # schedules identical at T (see above) share its figures
+        for T in Ts:
+            if c[3] and not one_pass[T]:
+                twin = (c[0], c[1], c[2], 0, c[4])
+                best_us[(c, T)], best_dsp[(c, T)] = best_us[(twin, T)], best_dsp[(twin, T)]
     ranked = sorted(valid, key=lambda c: sum(best_us[(c, T)] for T in Ts))
+
+    def best_at(T):
+        # the fastest schedule at T, the default kept unless another is faster by more than
+        # TIE (run-to-run spread); among schedules identical at T, the one without 'general'
+        pool = [c for c in valid if not (c[3] and not one_pass[T])]
+        c = min(pool, key=lambda c: best_us[(c, T)])
+        d = defaults[T]
+        if d in pool and best_us[(d, T)] <= best_us[(c, T)] * (1.0 + TIE):
+            return d
+        return c
+
+    best_T = {T: best_at(T) for T in Ts} if valid else {}
 
     lines = ["# Schedule tuning: %s" % args.workload, ""]
     if args.command:
         lines += ["Command (from the repository root):", "", "```", args.command.strip(), "```", ""]
-    lines += ["Shape H=%d E=%d I=%d k=%d; %d CUs; default schedule per T (kernel, grid, ring): %s. Latency: "
-              "mean of %d dispatch-stamped launches over %d rotated layers, best of %d repetitions." %
+    lines += ["Shape H=%d E=%d I=%d k=%d; %d CUs; default schedule per T (kernel/grid/ring): %s. Latency: per-launch "
+              "time of HIP graph replays holding one forward of each of %d rotated layers (median of %d replays), "
+              "best of %d repetitions; in brackets the mean dispatch-stamped launch time of the same launches. "
+              "Candidates: kernel/grid/ring, 'general' = passes of one token on the general single-tile kernel "
+              "instead of its one-token specialisation, 'R<=n' = multi-tile segment cap." %
               (cfg["H"], cfg["E"], cfg["I"], cfg["k"], info["num_cus"],
-               ", ".join("T=%d %s/%d/%d" % ((T,) + defaults[T]) for T in Ts), args.iters, args.layers, args.reps), "",
-              "| rank | kernel | grid | ring | " + " | ".join("T=%d us" % T for T in Ts) + " | sum us |",
-              "|---|---|---|---|" + "---|" * len(Ts) + "---|"]
+               ", ".join("T=%d %s" % (T, label(defaults[T])) for T in Ts), n, args.replays, args.reps), "",
+              "| rank | schedule | " + " | ".join("T=%d us" % T for T in Ts) + " | sum us |",
+              "|---|---|" + "---|" * len(Ts) + "---|"]
     for i, c in enumerate(ranked):
-        lines.append("| %d | %s | %d | %d | " % (i + 1, c[0], c[1], c[2]) +
-                     " | ".join("%.2f%s" % (best_us[(c, T)], "*" if defaults[T] == c else "") for T in Ts) +
+        lines.append("| %d | %s | " % (i + 1, label(c)) +
+                     " | ".join("%.2f (%.2f)%s" % (best_us[(c, T)], best_dsp[(c, T)], "*" if defaults[T] == c else "")
+                                for T in Ts) +
                      " | %.2f |" % sum(best_us[(c, T)] for T in Ts))
     for c, why in rejected.items():
-        lines.append("| rejected | %s | %d | %d | %s |" % (c[0], c[1], c[2], why))
-    best_T = {T: min(valid, key=lambda c: best_us[(c, T)]) for T in Ts} if valid else {}
-    lines += ["", "(* = the default schedule at that T.)", "",
-              "Best by sum: %s, grid %d, ring %d." % ranked[0] if ranked else "No valid schedule."]
+        lines.append("| rejected | %s | %s |" % (label(c), why))
+    lines += ["", "(* = the default schedule at that T; 'general' schedules at T without a pass of one token are "
+              "the same schedule as their twin and carry its figures.)", ""]
+    lines.append("Best by sum: %s." % label(ranked[0]) if ranked else "No valid schedule.")
     if best_T:
-        lines.append("Best per T: " + ", ".join("T=%d %s/%d/%d" % ((T,) + best_T[T]) for T in Ts) + ".")
+        lines.append("Best per T (the default unless another schedule is more than %d%% faster): " % round(TIE * 100)
+                     + ", ".join("T=%d %s" % (T, label(best_T[T])) for T in Ts) + ".")
     text = "\n".join(lines) + "\n"
     print(text, flush=True)
     if args.out:
         with open(args.out, "w") as fh:
             fh.write(text)
+    if args.table and best_T:
+        tab = load_table()
+        ent = tab.setdefault(args.workload, {})
+        for T, c in best_T.items():
+            grid = 0 if c[1] == info["num_cus"] else c[1]   # 0: one workgroup per CU, on any device
+            ent[str(T)] = dict(zip(SCHEDULE_KEYS, (c[0], grid, c[2], c[3], c[4])), us=round(best_us[(c, T)], 2),
+                               default_us=round(best_us[(defaults[T], T)], 2) if (defaults[T], T) in best_us else None)
+        with open(TABLE, "w") as fh:
+            json.dump(tab, fh, indent=1, sort_keys=True)
+            fh.write("\n")
     return 0
 
 
