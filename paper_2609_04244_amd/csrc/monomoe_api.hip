@@ -40,7 +40,6 @@ struct monomoe_plan_s {
     int grid;
     int lds_dyn;
     int lds_static;
-    int private_bytes;          // per-thread private (scratch) memory of the kernel
     int naq;
     int nslots;
     int tchunk;   // tokens per pass (T larger than one LDS-resident tile runs in passes)
@@ -191,10 +190,11 @@ int configure(const monomoe_plan_s* pl, int kernel, int ring, int group_cap, Ker
     if (ring != 0 && ring != pl->mtv->ring) return MONOMOE_OK;   // that depth exists in the single-tile kernel only
     KernelConfig m;
     if (config_multi(pl, group_cap, &m) == MONOMOE_OK) {
-        if (!sliced) {
-            *small = *c;
-            *small_T = c->tchunk;
-        }
+        // forwards that fit the single-tile kernel's tile stay on it; with a sliced down
+        // projection only forwards of one token do (its one-token specialisation is faster
+        // there, the multi-tile kernel from two tokens on)
+        *small = *c;
+        *small_T = sliced ? 1 : c->tchunk;
         *c = m;
     }
     return MONOMOE_OK;
@@ -234,13 +234,6 @@ int configure_plan(monomoe_plan_s* pl, int dev, int num_cus, int lds_total) {
     const int cr = configure(pl, MONOMOE_KERNEL_AUTO, 0, 0, &cfg, &small, &small_T);
     if (cr != MONOMOE_OK) return cr;
     apply_config(pl, cfg, small, small_T);
-    pl->private_bytes = 0;
-    for (const void* fn : {pl->var->fn, pl->var->fn1}) {
-        hipFuncAttributes attr;
-        if (!fn) continue;
-        if (hipFuncGetAttributes(&attr, fn) != hipSuccess) return MONOMOE_ERR_HIP;
-        pl->private_bytes = std::max(pl->private_bytes, (int)attr.localSizeBytes);
-    }
     pl->grid = pl->num_cus;   // one resident workgroup per CU
     if (pl->grid > kGridMax) return MONOMOE_ERR_UNSUPPORTED;
     return MONOMOE_OK;
@@ -658,22 +651,32 @@ int monomoe_plan_reset(monomoe_plan_t plan) {
 
 int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info) {
     if (!plan || !info) return MONOMOE_ERR_INVALID;
+    // the configuration a forward of the plan's T runs (the single-tile one when the
+    // multi-tile plan hands forwards of up to small_T tokens to it)
+    const KernelConfig& c = plan->shape.T <= plan->small_T ? plan->small : plan->cfg;
     info->grid = plan->grid;
     info->block = kThreads;
-    info->lds_bytes = plan->lds_dyn + plan->lds_static;
-    info->occupancy = plan->occupancy;
+    info->lds_bytes = c.lds_dyn + c.lds_static;
+    info->occupancy = c.occupancy;
     info->num_cus = plan->num_cus;
     info->workspace_bytes = (int64_t)plan->ws_bytes;
-    hipFuncAttributes attr;
-    info->scratch_bytes = hipFuncGetAttributes(&attr, plan->var->fn) == hipSuccess ? (int32_t)attr.localSizeBytes : -1;
-    if (plan->var->fn1 && info->scratch_bytes >= 0)   // and its one-token specialisation
-        info->scratch_bytes = hipFuncGetAttributes(&attr, plan->var->fn1) == hipSuccess
-                                  ? std::max(info->scratch_bytes, (int32_t)attr.localSizeBytes) : -1;
-    info->ring = plan->var->ring;
-    info->tokens_per_pass = plan->tchunk;
-    info->multi_tile = plan->mt;
-    info->group_tokens = plan->mt ? plan->mt_rows : 0;
-    info->down_slices = plan->mt ? (plan->shape.I / 128) / mt_slice_blocks(plan->shape.I / 128) : 1;
+    // scratch of every kernel the plan may launch (and the one-token specialisations)
+    info->scratch_bytes = 0;
+    const KernelVariant* vars[2] = {plan->cfg.var, plan->small_T > 0 ? plan->small.var : nullptr};
+    for (const KernelVariant* v : vars) {
+        if (!v) continue;
+        for (const void* fn : {v->fn, v->fn1}) {
+            hipFuncAttributes attr;
+            if (!fn || info->scratch_bytes < 0) continue;
+            info->scratch_bytes = hipFuncGetAttributes(&attr, fn) == hipSuccess
+                                      ? std::max(info->scratch_bytes, (int32_t)attr.localSizeBytes) : -1;
+        }
+    }
+    info->ring = c.var->ring;
+    info->tokens_per_pass = c.tchunk;
+    info->multi_tile = c.mt;
+    info->group_tokens = c.mt ? c.rows : 0;
+    info->down_slices = c.mt ? (plan->shape.I / 128) / mt_slice_blocks(plan->shape.I / 128) : 1;
     return MONOMOE_OK;
 }
 

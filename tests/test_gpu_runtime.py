@@ -54,7 +54,7 @@ def make_plan(inp, T):
     ("small_expert", 8, [8, 5, 1, 3, 0, 8]),
     ("small_expert", 24, [24, 16, 9, 1, 20]),   # the multi-tile kernel's plan; at most one tile: single-tile
     ("many_tiny_expert", 8, [2, 7, 4]),
-    ("coarse", 8, [1, 6, 8]),                   # sliced down projection: the multi-tile kernel at every T
+    ("coarse", 8, [1, 6, 8]),                   # sliced down projection: the multi-tile kernel from T = 2
 ])
 def test_runtime_token_count(name, Tplan, Ts):
     inp = wl.generate(wl.config(name), T=Tplan, seed=51, device=DEV)
@@ -72,10 +72,10 @@ def test_runtime_token_count(name, Tplan, Ts):
         if T == 0:
             continue
         check_output(inp, x, out)
-        # the single-tile kernel runs this call when the plan's kernel is single-tile, or when
-        # the call fits one tile and the down projection is not sliced; a plan built for T
-        # that also runs it computes the same bytes
-        single = info["multi_tile"] == 0 or (T <= 16 and info["down_slices"] == 1)
+        # the single-tile kernel runs this call when the plan's kernel is single-tile, when
+        # the call fits one tile and the down projection is not sliced, or when it has one
+        # token; a plan built for T that also runs it computes the same bytes
+        single = info["multi_tile"] == 0 or (T <= 16 and info["down_slices"] == 1) or T == 1
         ref_plan = make_plan(inp, T)
         if single and ref_plan.info()["multi_tile"] == 0:
             ref = ref_plan.forward(*args_of(inp, x))
