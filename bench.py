@@ -108,11 +108,13 @@ def measured_traffic(workload, kinds, TS):
     for path in sorted(glob.glob(os.path.join(PROFILES, "*_counters.json"))):
         with open(path) as fh:
             rec = json.load(fh)
-        kind = kernel_kind(rec.get("kernel", ""))
-        if rec.get("workload") != workload or rec.get("kernel_source_sha256") != kernel_source_hash(kind):
+        if rec.get("workload") != workload:
             continue
         for T, v in rec.get("per_T", {}).items():
-            if "fetch_bytes" in v and kinds.get(int(T)) == kind:
+            kind = kernel_kind(v.get("kernel", rec.get("kernel", "")))
+            hashes = rec.get("kernel_source_sha256_by_kind", {kernel_kind(rec.get("kernel", "")):
+                                                               rec.get("kernel_source_sha256")})
+            if "fetch_bytes" in v and kinds.get(int(T)) == kind and hashes.get(kind) == kernel_source_hash(kind):
                 per.setdefault(int(T), v["fetch_bytes"] + v["write_bytes"])
     if any(T not in per for T in TS):
         return None
@@ -266,6 +268,7 @@ class Workload:
         return {
             "layer": "%s: H=%d E=%d I=%d top-%d %s, block-FP8 128x128 weights, T in %s, %d rotated weight sets" % (
                 self.name, H, E, I, k, routing, list(self.TS), self.n),
+            "weight_sets": self.n,
             "value_GBps": round(float(value), 1), "frac_of_peak": round(float(value / PEAK_HBM_GBPS), 4),
             "launch_us_mean": round(float(tot_ms / n_launch * 1e3), 2),
             "ms_per_step": round(float(self.ms_per_step), 4),
@@ -357,13 +360,13 @@ def main():
         "metric": "routed-MoE op latency us + achieved HBM GB/s (% of peak) at T=" + ",".join(map(str, TS)) + " tokens",
         "value": round(float(value), 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(float(ms_per_step), 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "fp8_e4m3 operands (exact fp16 MFMA), fp32 accumulate",
+        "scaling": "weak", "vs_baseline": None, "dtype": "fp8_e4m3 operands (gate/up: exact fp16 MFMA, down: e4m3 MFMA), fp32 accumulate",
         "data": "synthetic",
         "config": {
             "workload": blk0["layer"],
             "other_workloads": [b["layer"] for n, b in blocks.items() if n != w0.name],
             "launches_per_step": len(TS) * len(wls), "grid": w0.plans[TS[0]].info()["grid"],
-            "block": w0.plans[TS[0]].info()["block"],
+            "block": w0.plans[TS[0]].info()["block"], "order": args.order,
             "step": "one forward per token count; each (layer, T) is timed over its own block of consecutive "
                     "launches (order %s); value, per_T and roofline are the headline layer's; ms_per_step sums "
                     "one launch of every T of every layer" % args.order,

@@ -7,8 +7,8 @@ are generated here beforehand and saved as raw little-endian binaries:
   generate:  draw `--layers` synthetic layers of a workload on the GPU and save
              DIR/l<l>_<field>.bin plus DIR/meta.txt ("H E I k renorm layers tmax has_bias");
   run:       the same launches from Python through the ctypes binding (no profiler needed);
-  bench:     summarise a --kernel-trace --stats run of bench.py itself: the fused kernel's
-             timed launches (the last --timed ones) against bench.py's own event timing;
+  bench:     summarise a --kernel-trace --stats run of bench.py itself: the headline layer's
+             timed launches per token count against bench.py's own event timing;
   timeline:  per-workgroup phase stamps of cold-cache launches (median and slowest
              workgroup per phase) beside the dispatch-stamped launch time;
   summarize: turn the CSV output of one --kernel-trace run and two --pmc runs (FETCH_SIZE,
@@ -174,17 +174,26 @@ def summarize(args):
     if len(fused) != n * len(Ts):
         raise SystemExit("expected %d fused launches in the trace, found %d" % (n * len(Ts), len(fused)))
     dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3   # us
-    kname = fused[0]["Kernel_Name"]
-    per_T = {}
+    per_T, names = {}, []
     for i, T in enumerate(Ts):
-        d = [dur(r) for r in fused[i * n:(i + 1) * n]]
-        per_T[T] = {"launches": n, "us_mean": sum(d) / n, "us_min": min(d), "us_max": max(d)}
+        rs = fused[i * n:(i + 1) * n]
+        if len({r["Kernel_Name"] for r in rs}) != 1:
+            raise SystemExit("T=%d: launches of more than one kernel" % T)
+        d = [dur(r) for r in rs]
+        per_T[T] = {"launches": n, "us_mean": sum(d) / n, "us_min": min(d), "us_max": max(d),
+                    "kernel": rs[0]["Kernel_Name"]}
+        names += [rs[0]["Kernel_Name"]] if rs[0]["Kernel_Name"] not in names else []
+    # the kernel of the largest T names the record; a plan's forwards of one token may run
+    # another one (the one-token specialisation), named per T
+    kname = per_T[Ts[-1]]["kernel"]
     nbytes = args.copy_mib << 20
     copy_us = min(dur(r) for r in copies) if copies else None
     read_us = min(dur(r) for r in reads) if reads else None
     rec = {
         "kernel": kname, "workload": args.workload, "token_counts": Ts, "launches_per_T": n,
-        "kernel_source_sha256": kernel_source_hash(kernel_kind(kname)), "per_T": {},
+        "kernel_source_sha256": kernel_source_hash(kernel_kind(kname)),
+        "kernel_source_sha256_by_kind": {k: kernel_source_hash(k) for k in sorted({kernel_kind(m) for m in names})},
+        "per_T": {},
         "copy_kernel": {"bytes_each_way": nbytes, "us_min": copy_us,
                         "GBps_read_plus_write": (2 * nbytes / copy_us / 1e3) if copy_us else None},
         "read_kernel": {"bytes": nbytes, "us_min": read_us,
@@ -243,13 +252,15 @@ def summarize(args):
     os.makedirs(os.path.dirname(os.path.abspath(args.out_json)), exist_ok=True)
     with open(args.out_json, "w") as fh:
         json.dump(rec, fh, indent=1)
-    lines = ["# %s on the %s workload" % (kname.split("(")[0], args.workload), "",
+    short = lambda m: m.split("(")[0].replace("void ", "")
+    lines = ["# %s on the %s workload" % (", ".join(short(m) for m in names), args.workload), "",
              "Command (from the repository root; DIR and OUT are scratch directories):", "", "```",
              args.command.strip(), "```", "",
-             "Kernel source sha256: `%s`" % rec["kernel_source_sha256"], "",
-             "| T | launches | mean us | min us | max us | HBM read (calibrated) | HBM write (calibrated) "
+             "Kernel source sha256: " + ", ".join("%s `%s`" % (k, h) for k, h in
+                                                  rec["kernel_source_sha256_by_kind"].items()), "",
+             "| T | kernel | launches | mean us | min us | max us | HBM read (calibrated) | HBM write (calibrated) "
              "| HBM GB/s (read+write / mean) | % of 8 TB/s |",
-             "|---|---|---|---|---|---|---|---|---|"]
+             "|---|---|---|---|---|---|---|---|---|---|"]
     for T in Ts:
         q = rec["per_T"][str(T)]
         rd = "%.1f MB" % (q["fetch_bytes"] / 1e6) if "fetch_bytes" in q else "-"
@@ -258,8 +269,9 @@ def summarize(args):
         if "fetch_bytes" in q and "write_bytes" in q:
             g = (q["fetch_bytes"] + q["write_bytes"]) / (q["us_mean"] * 1e-6) / 1e9
             bw, frac = "%.0f" % g, "%.1f" % (100.0 * g / 8000.0)
-        lines.append("| %d | %d | %.2f | %.2f | %.2f | %s | %s | %s | %s |" %
-                     (T, n, q["us_mean"], q["us_min"], q["us_max"], rd, wr, bw, frac))
+        lines.append("| %d | %s | %d | %.2f | %.2f | %.2f | %s | %s | %s | %s |" %
+                     (T, short(q["kernel"]).replace("monomoe::", ""), n, q["us_mean"], q["us_min"], q["us_max"],
+                      rd, wr, bw, frac))
     lines.append("")
     if copy_us:
         lines.append("Plain copy kernel, %d MiB each way: %.1f us (%.0f GB/s read+write)." %
@@ -295,43 +307,75 @@ def summarize(args):
 
 
 def bench_trace(args):
+    """The headline layer's timed launches in a kernel trace of bench.py, per token count,
+    beside bench.py's own dispatch-stamped times of the same launches.  The trace holds, in
+    dispatch order, the selection pass (one forward per weight set and T) and then, per T in
+    blocked order, warm-up and timed launches of consecutive weight sets; the other layers'
+    launches and the graph replays come after."""
     with open(_find(args.trace, "kernel_trace.csv")) as fh:
         tr = [r for r in csv.DictReader(fh) if "monomoe_fused" in r["Kernel_Name"]]
     tr.sort(key=lambda r: int(r["Dispatch_Id"]))
-    timed = tr[-args.timed:]
-    d = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in timed]
     with open(args.bench_json) as fh:
         b = json.loads(fh.read().strip().splitlines()[-1])
-    stats = [f for f in _rows(args.trace) if f.endswith("kernel_stats.csv")]
+    head = next(iter(b["workloads"].values()))
+    Ts = [int(t) for t in b["per_T"]]
+    steps, warmup, n = b["steps"], b["warmup"], head["weight_sets"]
+    if b["config"].get("order", "blocked") != "blocked":
+        raise SystemExit("the trace summary reads bench.py's blocked launch order")
+    H, I = (int(v) for v in head["kernel"].split("<")[1].rstrip(">").split(","))
+    sel = n * len(Ts)
+    per_T, names = {}, []
+    for i, T in enumerate(Ts):
+        start = sel + i * (warmup + steps) + warmup
+        rs = tr[start:start + steps]
+        if len(rs) != steps or any("<%d, %d," % (H, I) not in r["Kernel_Name"] for r in rs):
+            raise SystemExit("T=%d: the trace does not hold the headline layer's timed launches where "
+                             "bench.py's launch order puts them" % T)
+        d = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rs]
+        per_T[T] = sum(d) / len(d)
+        names += [rs[0]["Kernel_Name"]] if rs[0]["Kernel_Name"] not in names else []
+    kinds = sorted({kernel_kind(m) for m in names})
+    short = lambda m: m.split("(")[0].replace("void ", "").replace("monomoe::", "")
     lines = ["# bench.py under rocprofv3 --kernel-trace --stats", "",
              "Command (from the repository root; OUT is a scratch directory):", "", "```", args.command.strip(), "```", "",
-             "Kernel source sha256: `%s`" % kernel_source_hash(kernel_kind(tr[-1]["Kernel_Name"])), "",
-             "Fused-kernel launches in the trace: %d (selection pass, warm-up and timed); the last %d are the "
-             "timed ones." % (len(tr), len(timed)), "",
-             "| source | mean launch us |", "|---|---|",
-             "| rocprofv3 kernel trace, timed launches | %.2f |" % (sum(d) / len(d)),
-             "| bench.py dispatch-stamped HIP events, same (traced) run | %.2f |" % b["roofline"]["launch_us_mean"]]
+             "Kernel source sha256: " + ", ".join("%s `%s`" % (k, kernel_source_hash(k)) for k in kinds), "",
+             "Headline layer: %s." % head["layer"], "",
+             "Fused-kernel launches in the trace: %d (selection pass, warm-up, timed launches of every layer, graph "
+             "replays); per T the headline layer's %d timed launches sit after its selection pass (%d launches) "
+             "and, per T, %d warm-up launches." % (len(tr), steps, sel, warmup), ""]
+    un = None
     if args.untraced_json:
         with open(args.untraced_json) as fh:
-            u = json.loads(fh.read().strip().splitlines()[-1])
-        lines.append("| bench.py dispatch-stamped HIP events, run without the tracer | %.2f |" %
-                     u["roofline"]["launch_us_mean"])
+            un = json.loads(fh.read().strip().splitlines()[-1])
+    lines += ["| T | kernel | trace mean us | bench.py events, traced run, us | bench.py events, untraced run, us |",
+              "|---|---|---|---|---|"]
+    for i, T in enumerate(Ts):
+        start = sel + i * (warmup + steps) + warmup
+        lines.append("| %d | %s | %.2f | %.2f | %s |" % (
+            T, short(tr[start]["Kernel_Name"]), per_T[T], b["per_T"][str(T)]["us_mean"],
+            "%.2f" % un["per_T"][str(T)]["us_mean"] if un else "-"))
+    mean = sum(per_T.values()) / len(per_T)
+    lines.append("| mean | | %.2f | %.2f | %s |" % (mean, b["roofline"]["launch_us_mean"],
+                                                   "%.2f" % un["roofline"]["launch_us_mean"] if un else "-"))
     lines += ["", "(Under the tracer the event stamps include its own per-dispatch work; without it the "
               "dispatch-stamped events and the kernel trace agree.)", ""]
+
     def line(r):
         return "value %.1f GB/s (%.1f%% of 8 TB/s); per T: %s" % (
             r["value"], 100 * r["roofline"]["frac"],
             ", ".join("T=%s %.2f us" % (k, v["us_mean"]) for k, v in r["per_T"].items()))
     lines.append("bench.py line under the tracer: %s." % line(b))
-    if args.untraced_json:
-        lines += ["", "bench.py line without the tracer: %s." % line(u)]
+    if un:
+        lines += ["", "bench.py line without the tracer: %s." % line(un)]
+    stats = [f for f in _rows(args.trace) if f.endswith("kernel_stats.csv")]
     if stats:
         with open(stats[0]) as fh:
             rows = [r for r in csv.DictReader(fh)]
-        lines += ["", "rocprofv3 --stats (every launch of the process):", "",
+        lines += ["", "rocprofv3 --stats (every launch of the process, the fused kernels first):", "",
                   "| kernel | calls | average ns | min ns | max ns |", "|---|---|---|---|---|"]
-        for r in rows[:8]:
-            lines.append("| %s | %s | %s | %s | %s |" % (r.get("Name", "")[:60], r.get("Calls", ""),
+        rows.sort(key=lambda r: "monomoe_fused" not in r.get("Name", ""))
+        for r in rows[:10]:
+            lines.append("| %s | %s | %s | %s | %s |" % (short(r.get("Name", ""))[:60], r.get("Calls", ""),
                          r.get("AverageNs", ""), r.get("MinNs", ""), r.get("MaxNs", "")))
     with open(args.out_md, "w") as fh:
         fh.write("\n".join(lines) + "\n")
@@ -476,7 +520,6 @@ def main():
     m.add_argument("--out-json", required=True)
     bt = sub.add_parser("bench")
     bt.add_argument("--trace", required=True)
-    bt.add_argument("--timed", type=int, required=True, help="timed launches (steps x token counts)")
     bt.add_argument("--bench-json", required=True, help="bench.py's output line")
     bt.add_argument("--untraced-json", help="bench.py's output line from a run without the tracer")
     bt.add_argument("--command", default="")
