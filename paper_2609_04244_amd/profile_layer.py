@@ -11,6 +11,7 @@ are generated here beforehand and saved as raw little-endian binaries:
              timed launches per token count against bench.py's own event timing;
   timeline:  per-workgroup phase stamps of cold-cache launches (median and slowest
              workgroup per phase) beside the dispatch-stamped launch time;
+  compare:   two summarize records of one workload side by side (launch time and counters);
   summarize: turn the CSV output of one --kernel-trace run and two --pmc runs (FETCH_SIZE,
              WRITE_SIZE) of the C++ driver into a markdown summary and a JSON record: mean
              launch duration per token count, HBM bytes per launch from the counters scaled by
@@ -126,11 +127,14 @@ def kernel_kind(kernel_name):
     return "multi" if "monomoe_fused_mt" in kernel_name else "single"
 
 
-def kernel_source_hash(kind="single"):
-    """sha256 over one kernel's sources."""
+def kernel_source_hash(kind="single", root=None):
+    """sha256 over one kernel's sources in this package, or over those of them that exist in
+    the package directory `root` of another checkout (an older one may have fewer files)."""
     h = hashlib.sha256()
-    here = os.path.dirname(os.path.abspath(__file__))
+    here = root or os.path.dirname(os.path.abspath(__file__))
     for f in KERNEL_SOURCES[kind]:
+        if root and not os.path.exists(os.path.join(here, f)):
+            continue
         with open(os.path.join(here, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
@@ -191,8 +195,9 @@ def summarize(args):
     read_us = min(dur(r) for r in reads) if reads else None
     rec = {
         "kernel": kname, "workload": args.workload, "token_counts": Ts, "launches_per_T": n,
-        "kernel_source_sha256": kernel_source_hash(kernel_kind(kname)),
-        "kernel_source_sha256_by_kind": {k: kernel_source_hash(k) for k in sorted({kernel_kind(m) for m in names})},
+        "kernel_source_sha256": kernel_source_hash(kernel_kind(kname), args.sources),
+        "kernel_source_sha256_by_kind": {k: kernel_source_hash(k, args.sources)
+                                         for k in sorted({kernel_kind(m) for m in names})},
         "per_T": {},
         "copy_kernel": {"bytes_each_way": nbytes, "us_min": copy_us,
                         "GBps_read_plus_write": (2 * nbytes / copy_us / 1e3) if copy_us else None},
@@ -382,6 +387,43 @@ def bench_trace(args):
     print("\n".join(lines))
 
 
+def compare(args):
+    """Two summarize records of one workload side by side: mean launch time and every
+    counter both hold, per token count both hold, with the relative change."""
+    recs = []
+    for path in (args.before, args.after):
+        with open(path) as fh:
+            recs.append(json.load(fh))
+    a, b = recs
+    Ts = [T for T in a["per_T"] if T in b["per_T"]]
+    names = [n for n in a["per_T"][Ts[0]].get("counters", {}) if n in b["per_T"][Ts[0]].get("counters", {})]
+    short = lambda m: m.split("(")[0].replace("void ", "").replace("monomoe::", "")
+    lines = ["# %s: %s against %s" % (a["workload"], args.label_after, args.label_before), "",
+             "Commands (from the repository root):", "", "```", args.command.strip(), "```", ""]
+    for label, r in ((args.label_before, a), (args.label_after, b)):
+        lines.append("- %s: kernel source sha256 %s." % (label, ", ".join(
+            "%s `%s`" % kv for kv in r.get("kernel_source_sha256_by_kind",
+                                           {kernel_kind(r["kernel"]): r["kernel_source_sha256"]}).items())))
+    lines += ["", "Mean per launch (rocprofv3 sums counters over the device); change = after / before - 1.", ""]
+    if args.note:
+        lines += [args.note, ""]
+    for T in Ts:
+        qa, qb = a["per_T"][T], b["per_T"][T]
+        lines += ["## T=%s" % T, "",
+                  "| quantity | %s | %s | change |" % (args.label_before, args.label_after), "|---|---|---|---|",
+                  "| kernel | %s | %s | |" % (short(qa.get("kernel", a["kernel"])), short(qb.get("kernel", b["kernel"]))),
+                  "| launch us (kernel trace mean) | %.2f | %.2f | %+.1f%% |" % (
+                      qa["us_mean"], qb["us_mean"], 100 * (qb["us_mean"] / qa["us_mean"] - 1))]
+        for n in names:
+            va, vb = qa["counters"][n], qb["counters"][n]
+            lines.append("| %s | %.4g | %.4g | %s |" % (n, va, vb, "%+.1f%%" % (100 * (vb / va - 1)) if va else "-"))
+        lines.append("")
+    text = "\n".join(lines)
+    with open(args.out_md, "w") as fh:
+        fh.write(text)
+    print(text)
+
+
 # Phase stamps of the kernels (the kSt* indices of csrc/monomoe_internal.h), in the order
 # the phases happen; the label says which wavefront stamps it.
 STAMPS = [
@@ -389,7 +431,7 @@ STAMPS = [
     (12, "input quantised (LDS)"),
     (15, "all logits of token 0 seen (wave 0)"),
     (16, "token 0 selected (wave 0)"),
-    (13, "top-k barrier passed"),
+    (13, "top-k done (barrier passed; one-token kernel: last expert ranked)"),
     (19, "expert token masks built"),
     (3, "routing metadata built"),
     (17, "work partition found (wave 0)"),
@@ -518,6 +560,16 @@ def main():
     m.add_argument("--command", default="", help="the command lines that produced the runs")
     m.add_argument("--out-md", required=True)
     m.add_argument("--out-json", required=True)
+    m.add_argument("--sources", help="package directory whose kernel sources the runs were built from "
+                                     "(default: this package)")
+    c = sub.add_parser("compare")
+    c.add_argument("--before", required=True, help="summarize record (JSON)")
+    c.add_argument("--after", required=True, help="summarize record (JSON)")
+    c.add_argument("--label-before", default="before")
+    c.add_argument("--label-after", default="after")
+    c.add_argument("--command", default="")
+    c.add_argument("--note", default="", help="a paragraph printed above the tables")
+    c.add_argument("--out-md", required=True)
     bt = sub.add_parser("bench")
     bt.add_argument("--trace", required=True)
     bt.add_argument("--bench-json", required=True, help="bench.py's output line")
@@ -538,6 +590,8 @@ def main():
         timeline(args)
     elif args.cmd == "bench":
         bench_trace(args)
+    elif args.cmd == "compare":
+        compare(args)
     elif args.cmd == "generate":
         generate(args)
     elif args.cmd == "run":
