@@ -223,8 +223,13 @@ __device__ __forceinline__ v4f block_mma_f8(const v4i& a0, const v4i& a1, const 
                                                             kMfmaScaleOne);
 }
 
-// Bounded wait until *p >= target on an LDS flag; false on abort or timeout.
-static __device__ bool wait_lds(const int* p, int target, const int* abort_flag, uint64_t limit) {
+// Bounded wait until *p >= target on an LDS flag; false on abort or timeout.  Inlined where
+// a translation unit asks for it (a call from a streaming loop costs a register save and
+// restore around it); a call elsewhere.
+#ifndef MONOMOE_WAIT_INLINE
+#define MONOMOE_WAIT_INLINE
+#endif
+static __device__ MONOMOE_WAIT_INLINE bool wait_lds(const int* p, int target, const int* abort_flag, uint64_t limit) {
     if (lds_ld(p) >= target) {
         compiler_fence();   // the data the flag guards is read after it
         return true;

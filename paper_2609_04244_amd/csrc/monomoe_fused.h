@@ -54,9 +54,9 @@
 
 #include "monomoe_device.h"
 
-// Inlining of the weight-load cursor's helpers (lbase, lnext): forced in a translation unit
-// whose inliner would otherwise outline them (a call from the streaming loop spills the
-// weight ring to scratch); left to the compiler elsewhere.
+// Inlining of the weight-load cursor's helpers (lbase, lnext, ranked): forced by the
+// translation units of the kernel (a call from the streaming loop spills the weight ring
+// to scratch); left to the compiler elsewhere.
 #ifndef MONOMOE_CURSOR_INLINE
 #define MONOMOE_CURSOR_INLINE
 #endif
@@ -68,8 +68,9 @@ namespace monomoe {
 // over j in top-k order, polled until all carry this launch's tag, then rounded to bf16
 // (the fp32 sum also goes to the test hook).  One wavefront, lane l owns output o0 + l.
 // False on timeout or when another workgroup has recorded an error.
+// (Always inlined: a call would pass the kernel's argument block through scratch memory.)
 template <int H>
-__device__ bool reduce_chunk(const KParams& p, int ht, int o0, int T, int K, uint32_t tag, int lane,
+__device__ __attribute__((always_inline)) bool reduce_chunk(const KParams& p, int ht, int o0, int T, int K, uint32_t tag, int lane,
                              uint32_t* status, uint64_t limit) {
     const uint64_t t0 = now();
     const int o = min(o0 + lane, T * 16 - 1);
@@ -312,15 +313,21 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
     }
 
     // ---------------- work partition (identical in every wavefront) ----------------
+    // Gate/up units are dealt round-robin over the workgroups: the j-th unit of workgroup
+    // wg is unit wg + G*j.  Each expert's units are spread over many workgroups and every
+    // workgroup works through the experts in slot order, so all workgroups stream the same
+    // few experts at a time and the act rows complete expert by expert through the phase
+    // (and with one token every workgroup starts on one of the first selections).  Down
+    // units are split into contiguous ranges (one or two experts per workgroup, so each
+    // workgroup requantises one or two act rows).
     const int n_up = U * UPE, n_dn = U * DNE;
-    // (products below 2^32: U <= kUMax, G <= kGridMax)
-    static_assert((uint64_t)kUMax * (I / 8) * kGridMax < (1ull << 32) &&
-                      (uint64_t)kUMax * (H / 16) * kGridMax < (1ull << 32), "partition arithmetic");
-    const uint32_t g32 = (uint32_t)G, w32 = (uint32_t)wg;
-    const int ulo = (int)(w32 * (uint32_t)n_up / g32), uhi = (int)((w32 + 1) * (uint32_t)n_up / g32);
-    const int dlo = (int)(w32 * (uint32_t)n_dn / g32), dhi = (int)((w32 + 1) * (uint32_t)n_dn / g32);
-    const int nu = uhi - ulo, nd = dhi - dlo;
-    const int dn_u0 = nd > 0 ? dlo / DNE : 0;   // first expert slot of the down range
+    static_assert((uint64_t)kUMax * (H / 16) * kGridMax < (1ull << 32) &&
+                      (uint64_t)kUMax * (I / 8) + kGridMax < (1ull << 31), "partition arithmetic");
+    const int nu = n_up > wg ? (n_up - 1 - wg) / G + 1 : 0;   // gate/up units of this workgroup
+    const int dlo = (int)((uint32_t)wg * (uint32_t)n_dn / (uint32_t)G);
+    const int dhi = (int)((uint32_t)(wg + 1) * (uint32_t)n_dn / (uint32_t)G);
+    const int nd = dhi - dlo;                                 // down units of this workgroup
+    const int dn_u0 = nd > 0 ? dlo / DNE : 0;                 // first expert slot of the down range
 
     if (ok && wv < NC) {
         // ====================== compute wavefronts ======================
@@ -349,42 +356,50 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
             kp0 = (NP % NC == 0) ? wv : ((wv - r * NP) & (NC - 1));
             return (NP % NC == 0) ? NP / NC : (NP - 1 - kp0) / NC + 1;
         };
-        // the first unit >= m of a phase starting at lo in which this wave has tasks
-        auto own = [&](int m, int lo, int NP) -> int { return NP < NC ? m + ((wv - (m - lo)) & (NC - 1)) : m; };
+        // the first unit >= m of a phase (units are this workgroup's sequence numbers in the
+        // phase) in which this wave has tasks
+        auto own = [&](int m, int NP) -> int { return NP < NC ? m + ((wv - m) & (NC - 1)) : m; };
         // from (ph, m) on, the first unit in which this wave has tasks (ph = 2: none left);
         // closed form, no search; returned by value so the cursors stay in registers
         struct Pos { int ph, m, kp, cnt; };
         auto seek = [&](int ph, int m) -> Pos {
             if (ph == 0) {
-                m = own(m, ulo, HP);
-                if (m < uhi) {
+                m = own(m, HP);
+                if (m < nu) {
                     int kp;
-                    const int cnt = share(m - ulo, HP, kp);
+                    const int cnt = share(m, HP, kp);
                     return Pos{0, m, kp, cnt};
                 }
-                m = dlo;
+                m = 0;
             }
             if (ph <= 1) {
-                m = own(m, dlo, IP);
-                if (m < dhi) {
+                m = own(m, IP);
+                if (m < nd) {
                     int kp;
-                    const int cnt = share(m - dlo, IP, kp);
+                    const int cnt = share(m, IP, kp);
                     return Pos{1, m, kp, cnt};
                 }
             }
             return Pos{2, m, 0, 0};
         };
-        // One-token path: wait until the selections of this workgroup's last slot are published
-        // (slots are top-k positions, so the first workgroups' experts are known first).  An
-        // undetermined selection (-1) is reported by the helper; its address is clamped here.
-        if constexpr (ONE) {
-            const int need = max(nu > 0 ? (uhi - 1) / UPE : -1, nd > 0 ? (dhi - 1) / DNE : -1) + 1;
-            if (need > 0 && !wait_lds(&f_rank, need, &f_abort, limit)) {
-                set_status(status, kDevTimeout);
-                lds_st(&f_abort, 1);   // the waits that follow see the abort
+        // One-token path: before the first load of a unit of expert slot u, wait until the
+        // selection of slot u is published (slots are top-k positions, ranked in order).  An
+        // undetermined selection (-1) is reported by the helper; its address is clamped.
+        auto ranked = [&](int u) MONOMOE_CURSOR_INLINE {
+            if (lds_ld(&f_rank) <= u) {
+                const uint64_t t0 = now();
+                while (lds_ld(&f_rank) <= u) {
+                    if (lds_ld(&f_abort) || now() - t0 > limit) {
+                        set_status(status, kDevTimeout);
+                        lds_st(&f_abort, 1);   // the waits that follow see the abort
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+                }
             }
-        }
-        const Pos p0 = seek(0, ulo);
+            compiler_fence();   // the selection is read after its counter
+        };
+        const Pos p0 = seek(0, 0);
         const int ph0 = p0.ph, m0 = p0.m, kp00 = p0.kp, cnt0 = p0.cnt;
         if (wv == 0 && lane == 0) stamp(p.stamps, wg, kStSeek);
 
@@ -397,7 +412,9 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
         auto lbase = [&]() MONOMOE_CURSOR_INLINE {   // per-lane addresses of task lkp of unit lm
             const int kb = 2 * lkp;
             if (lph == 0) {
-                const int u = lm / UPE, i0 = (lm - u * UPE) * 8;
+                const int mu = wg + G * lm;   // the unit
+                const int u = mu / UPE, i0 = (mu - u * UPE) * 8;
+                if constexpr (ONE) ranked(u);
                 const int e = ONE ? min(max(uni(sel_ids[u]), 0), E - 1) : uni(act_e[u]);
                 const int row = (r16 < 8) ? (i0 + r16) : (I + i0 + r16 - 8);
                 lptr = p.w13 + ((size_t)e * 2 * I + row) * H + kb * 128 + kq * 16;
@@ -407,7 +424,9 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
                 lstep = (HP < NC) ? 256 : kTaskA;
                 lsstep = (HP < NC) ? 2 : NC * 2;
             } else {
-                const int u = lm / DNE, ht = lm - u * DNE;
+                const int mu = dlo + lm;   // the unit
+                const int u = mu / DNE, ht = mu - u * DNE;
+                if constexpr (ONE) ranked(u);
                 const int e = ONE ? min(max(uni(sel_ids[u]), 0), E - 1) : uni(act_e[u]);
                 lptr = p.w2 + ((size_t)e * H + ht * 16 + r16) * I + kb * 128 + kq * 16;
                 lso = (uint32_t)((e * HB + (ht >> 3)) * IB + kb);
@@ -467,8 +486,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
                 bstep = (HP < NC) ? 256 : kTaskA;
                 sstep = (HP < NC) ? 2 : NC * 2;
             } else {
-                const int u = cm / DNE;
-                const int x = u - dn_u0;
+                const int x = (dlo + cm) / DNE - dn_u0;   // this workgroup's x-th expert
                 const int buf = (naq == 2) ? (x & 1) : 0;
                 if (!wait_lds(&f_aq_seq[buf], x + 1, &f_abort, limit)) return false;
                 const uint8_t* aq_s = lds_dyn + buf * aq_bytes;
@@ -481,7 +499,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
         };
         bool stamped = false;
         auto handoff = [&](const v4f& acc) -> bool {   // partial sums of unit cm to the helper
-            const int useq = (cph == 0) ? (cm - ulo) : (nu + cm - dlo);
+            const int useq = (cph == 0) ? cm : (nu + cm);
             const int slot = useq & smask;
             if (!wait_lds(&f_consumed, useq - smask, &f_abort, limit)) return false;
             part[(slot * NC + wv) * 64 + lane] = acc;
@@ -575,7 +593,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
 
         // --- gate/up epilogues: SiLU(gate)*up, stored as tagged words ---
         for (int j = 0; j < nu; ++j) {
-            const int m = ulo + j, slot = j & smask;
+            const int m = wg + G * j, slot = j & smask;
             if (!wait_lds(&f_cnt[slot], NCU, &f_abort, limit)) { fine = false; break; }
             const int u = m / UPE, i0 = (m - u * UPE) * 8;
             const uint32_t tmask = act_m[u];

@@ -314,8 +314,8 @@ def summarize(args):
 def bench_trace(args):
     """The headline layer's timed launches in a kernel trace of bench.py, per token count,
     beside bench.py's own dispatch-stamped times of the same launches.  The trace holds, in
-    dispatch order, the selection pass (one forward per weight set and T) and then, per T in
-    blocked order, warm-up and timed launches of consecutive weight sets; the other layers'
+    dispatch order, every layer's selection pass (one forward per weight set and T), then the
+    headline layer's warm-up and timed launches per T in blocked order; the other layers'
     launches and the graph replays come after."""
     with open(_find(args.trace, "kernel_trace.csv")) as fh:
         tr = [r for r in csv.DictReader(fh) if "monomoe_fused" in r["Kernel_Name"]]
@@ -328,7 +328,7 @@ def bench_trace(args):
     if b["config"].get("order", "blocked") != "blocked":
         raise SystemExit("the trace summary reads bench.py's blocked launch order")
     H, I = (int(v) for v in head["kernel"].split("<")[1].rstrip(">").split(","))
-    sel = n * len(Ts)
+    sel = sum(w["weight_sets"] for w in b["workloads"].values()) * len(Ts)   # every layer's selection pass
     per_T, names = {}, []
     for i, T in enumerate(Ts):
         start = sel + i * (warmup + steps) + warmup
@@ -346,7 +346,7 @@ def bench_trace(args):
              "Kernel source sha256: " + ", ".join("%s `%s`" % (k, kernel_source_hash(k)) for k in kinds), "",
              "Headline layer: %s." % head["layer"], "",
              "Fused-kernel launches in the trace: %d (selection pass, warm-up, timed launches of every layer, graph "
-             "replays); per T the headline layer's %d timed launches sit after its selection pass (%d launches) "
+             "replays); per T the headline layer's %d timed launches sit after the selection passes (%d launches) "
              "and, per T, %d warm-up launches." % (len(tr), steps, sel, warmup), ""]
     un = None
     if args.untraced_json:

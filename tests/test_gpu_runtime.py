@@ -142,16 +142,26 @@ def test_graph_capture_and_replay(name, T):
 def test_plans_created_in_descending_footprint():
     # the dynamic-LDS limit of a kernel symbol is shared by every plan: a later plan with a
     # smaller footprint must not break the launches of an earlier, larger one
-    inp = wl.generate(wl.config("small_expert"), T=8, seed=71, device=DEV)
-    big = make_plan(inp, 8)
-    small = make_plan(inp, 1)
-    log("LDS per workgroup: T=8 plan %d, T=1 plan %d" % (big.info()["lds_bytes"], small.info()["lds_bytes"]))
-    assert big.info()["lds_bytes"] > small.info()["lds_bytes"]
-    run_case(inp, plan=big)
-    d1 = dict(inp)
-    d1["x"] = inp["x"][:1].contiguous()
-    d1["T"] = 1
-    run_case(d1, plan=small)
-    run_case(inp, plan=big)
+    inp = wl.generate(wl.config("small_expert"), T=16, seed=71, device=DEV)
+    Ts = (1, 2, 4, 8, 16)
+    lds = {}
+    for T in Ts:
+        q = make_plan(inp, T)
+        lds[T] = q.info()["lds_bytes"]
+        q.close()
+    Tb, Tsm = max(Ts, key=lambda T: lds[T]), min(Ts, key=lambda T: lds[T])
+    log("LDS per workgroup by T: %s; larger plan T=%d, smaller T=%d" % (lds, Tb, Tsm))
+    assert lds[Tb] > lds[Tsm]
+    big = make_plan(inp, Tb)
+    small = make_plan(inp, Tsm)
+
+    def case(T):
+        d = dict(inp)
+        d["x"] = inp["x"][:T].contiguous()
+        d["T"] = T
+        return d
+    run_case(case(Tb), plan=big)
+    run_case(case(Tsm), plan=small)
+    run_case(case(Tb), plan=big)
     small.close()
     big.close()
