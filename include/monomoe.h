@@ -269,6 +269,30 @@ typedef struct {
 } monomoe_schedule_t;
 int monomoe_plan_set_schedule(monomoe_plan_t plan, const monomoe_schedule_t* sched);
 
+/* Layout of a kernel's LDS for a shape, and the residency check, computed on the host
+ * without a device (no HIP call, no allocation): what monomoe_plan and
+ * monomoe_plan_set_schedule configure, for capacity planning and for tests of the
+ * refusals.  `shape` and `topk` as for monomoe_plan (shape->T: tokens per forward);
+ * `kernel` MONOMOE_KERNEL_SINGLE or MONOMOE_KERNEL_MULTI; `lds_total` the LDS bytes a
+ * workgroup may use on the device and `lds_static` the kernel's own static LDS;
+ * `occupancy` the workgroups per CU that the device's occupancy query reports for the
+ * resulting layout; `grid` the persistent workgroups (0: one per CU) on `num_cus` CUs.
+ * Returns MONOMOE_ERR_INVALID / MONOMOE_ERR_UNSUPPORTED for the arguments monomoe_plan
+ * refuses and for bad sizes, MONOMOE_ERR_UNSUPPORTED when no layout fits the LDS, else
+ * fills *out and returns MONOMOE_ERR_OCCUPANCY when the grid cannot be resident at once
+ * (occupancy < 1, or grid > num_cus * occupancy: the kernel's cross-workgroup waits need
+ * every workgroup resident; Sec. 3.2, persistent residency), MONOMOE_OK otherwise. */
+typedef struct {
+    int32_t tokens_per_pass; /* token tile of one pass (multi-tile: T)             */
+    int32_t group_tokens;    /* multi-tile: tokens per segment R; single-tile: 0   */
+    int32_t act_buffers;     /* requantised-activation LDS buffers                  */
+    int32_t handoff_slots;   /* partial-sum hand-off slots between the wavefronts   */
+    int32_t lds_bytes;       /* dynamic LDS per workgroup                           */
+} monomoe_layout_t;
+
+int monomoe_layout(const monomoe_shape_t* shape, int topk, int kernel, int lds_total, int lds_static,
+                   int occupancy, int grid, int num_cus, monomoe_layout_t* out);
+
 /* 1 if (H, I) is one of the compiled shapes, else 0. */
 int monomoe_supported_shape(int32_t H, int32_t I);
 

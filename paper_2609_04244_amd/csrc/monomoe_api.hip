@@ -86,6 +86,55 @@ hipError_t allow_full_lds(const void* fn, int lds_total, const hipFuncAttributes
 // many partial-sum slots as the rest of the LDS holds (more slots let the compute
 // wavefronts run further ahead of the helper's epilogues).  Every ring depth must fit, so
 // schedules can switch.
+// Host arithmetic of the layouts and of residency (no device call), shared by plan
+// creation and monomoe_layout.
+//
+// Single-tile kernel, T tokens, lds_cap bytes of dynamic LDS: the largest token tile (a
+// pass) that fits with one act buffer and the minimum of hand-off slots, the act double
+// buffered when that fits too, then as many slots (a power of two) as fit.
+int single_layout(int H, int I, int T, int lds_cap, KernelConfig* k) {
+    int Tl = std::min(std::max(T, 1), kTMax);
+    while (Tl > 1 && lds_dynamic_bytes(H, I, Tl, 1, kSlotsMin) > lds_cap) --Tl;
+    k->tchunk = Tl;
+    k->naq = lds_dynamic_bytes(H, I, Tl, 2, kSlotsMin) <= lds_cap ? 2 : 1;
+    k->nslots = kSlotsMin;
+    while (k->nslots < kSlotsMax && lds_dynamic_bytes(H, I, Tl, k->naq, k->nslots * 2) <= lds_cap) k->nslots *= 2;
+    k->lds_dyn = lds_dynamic_bytes(H, I, Tl, k->naq, k->nslots);
+    return k->lds_dyn > lds_cap ? MONOMOE_ERR_UNSUPPORTED : MONOMOE_OK;
+}
+
+// Multi-tile kernel: the largest segment size R (<= T, <= group_cap when nonzero) whose
+// LDS layout fits, then as many quantised-input ring rows as the rest holds.  Segments
+// per forward are bounded by min(E, T*k) + ceil(T*k / R), which must fit the kernel's
+// segment queue.
+int multi_layout(int H, int I, int T, int E, int topk, int group_cap, int lds_cap, KernelConfig* k) {
+    T = std::max(T, 1);
+    int R = std::min(T, kTLimit);
+    if (group_cap > 0) R = std::min(R, group_cap);
+    for (; R >= 1; --R) {
+        k->tiles = (R + 15) / 16;
+        if (mt_region_bytes(H, I, R, R) + mt_partials_bytes(kSlotsMin, k->tiles) <= lds_cap) break;
+    }
+    if (R < 1) return MONOMOE_ERR_UNSUPPORTED;
+    k->rows = R;
+    k->pool = R;
+    while (k->pool < 1024 && mt_region_bytes(H, I, k->pool + 1, R) + mt_partials_bytes(kSlotsMin, k->tiles) <= lds_cap)
+        ++k->pool;
+    const int pairs = T * topk;
+    if (std::min(E, pairs) + (pairs + R - 1) / R > kQMax) return MONOMOE_ERR_UNSUPPORTED;
+    k->naq = 2;
+    k->nslots = kSlotsMin;
+    k->tchunk = T;
+    k->lds_dyn = mt_region_bytes(H, I, k->pool, R) + mt_partials_bytes(k->nslots, k->tiles);
+    return MONOMOE_OK;
+}
+
+// A persistent grid waits across workgroups, so all of its workgroups must be resident at
+// once: grid <= num_cus * occupancy (workgroups per CU the layout allows).
+int residency(int occupancy, int grid, int num_cus) {
+    return (occupancy < 1 || (int64_t)grid > (int64_t)num_cus * occupancy) ? MONOMOE_ERR_OCCUPANCY : MONOMOE_OK;
+}
+
 int config_single(const monomoe_plan_s* pl, int ring, KernelConfig* c) {
     const monomoe_shape_t& s = pl->shape;
     const KernelVariant* var = nullptr;
@@ -97,15 +146,8 @@ int config_single(const monomoe_plan_s* pl, int ring, KernelConfig* c) {
     KernelConfig k{};
     k.var = var;
     k.lds_static = (int)attr.sharedSizeBytes;
-    const int lds_cap = pl->lds_total - k.lds_static;
-    int Tl = std::min(std::max(s.T, 1), kTMax);
-    while (Tl > 1 && lds_dynamic_bytes(s.H, s.I, Tl, 1, kSlotsMin) > lds_cap) --Tl;
-    k.tchunk = Tl;
-    k.naq = lds_dynamic_bytes(s.H, s.I, Tl, 2, kSlotsMin) <= lds_cap ? 2 : 1;
-    k.nslots = kSlotsMin;
-    while (k.nslots < kSlotsMax && lds_dynamic_bytes(s.H, s.I, Tl, k.naq, k.nslots * 2) <= lds_cap) k.nslots *= 2;
-    k.lds_dyn = lds_dynamic_bytes(s.H, s.I, Tl, k.naq, k.nslots);
-    if (k.lds_dyn > lds_cap) return MONOMOE_ERR_UNSUPPORTED;
+    const int lr = single_layout(s.H, s.I, s.T, pl->lds_total - k.lds_static, &k);
+    if (lr != MONOMOE_OK) return lr;
     k.occupancy = 0;
     for (const KernelVariant& v : pl->kern->v) {
         for (const void* fn : {v.fn, v.fn1}) {   // the kernel and its one-token specialisation
@@ -116,7 +158,7 @@ int config_single(const monomoe_plan_s* pl, int ring, KernelConfig* c) {
                 hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, fn, kThreads, (size_t)k.lds_dyn) != hipSuccess)
                 return MONOMOE_ERR_HIP;
             if ((int)va.sharedSizeBytes + k.lds_dyn > pl->lds_total) return MONOMOE_ERR_UNSUPPORTED;
-            if (o < 1) return MONOMOE_ERR_OCCUPANCY;
+            if (residency(o, pl->num_cus, pl->num_cus) != MONOMOE_OK) return MONOMOE_ERR_OCCUPANCY;
             if (&v == var) k.occupancy = k.occupancy ? std::min(k.occupancy, o) : o;
         }
     }
@@ -124,9 +166,7 @@ int config_single(const monomoe_plan_s* pl, int ring, KernelConfig* c) {
     return MONOMOE_OK;
 }
 
-// Multi-tile kernel: the largest segment size R (<= T, <= group_cap when nonzero) whose
-// LDS layout fits, then as many quantised-input ring rows as the rest holds.  Segments
-// per forward are bounded by min(E, T*k) + ceil(T*k / R).
+// Multi-tile kernel configuration of a plan (layout: multi_layout).
 int config_multi(const monomoe_plan_s* pl, int group_cap, KernelConfig* c) {
     const monomoe_shape_t& s = pl->shape;
     if (!pl->mtv) return MONOMOE_ERR_UNSUPPORTED;
@@ -136,30 +176,13 @@ int config_multi(const monomoe_plan_s* pl, int group_cap, KernelConfig* c) {
     k.var = pl->mtv;
     k.mt = 1;
     k.lds_static = (int)attr.sharedSizeBytes;
-    const int lds_cap = pl->lds_total - k.lds_static;
-    const int T = std::max(s.T, 1);
-    int R = std::min(T, kTLimit);
-    if (group_cap > 0) R = std::min(R, group_cap);
-    for (; R >= 1; --R) {
-        k.tiles = (R + 15) / 16;
-        if (mt_region_bytes(s.H, s.I, R, R) + mt_partials_bytes(kSlotsMin, k.tiles) <= lds_cap) break;
-    }
-    if (R < 1) return MONOMOE_ERR_UNSUPPORTED;
-    k.rows = R;
-    k.pool = R;
-    while (k.pool < 1024 && mt_region_bytes(s.H, s.I, k.pool + 1, R) + mt_partials_bytes(kSlotsMin, k.tiles) <= lds_cap)
-        ++k.pool;
-    const int pairs = T * pl->topk;
-    if (std::min(s.E, pairs) + (pairs + R - 1) / R > kQMax) return MONOMOE_ERR_UNSUPPORTED;
-    k.naq = 2;
-    k.nslots = kSlotsMin;
-    k.tchunk = T;
-    k.lds_dyn = mt_region_bytes(s.H, s.I, k.pool, R) + mt_partials_bytes(k.nslots, k.tiles);
+    const int lr = multi_layout(s.H, s.I, s.T, s.E, pl->topk, group_cap, pl->lds_total - k.lds_static, &k);
+    if (lr != MONOMOE_OK) return lr;
     int o = 0;
     if (allow_full_lds(k.var->fn, pl->lds_total, &attr) != hipSuccess ||
         hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, k.var->fn, kThreads, (size_t)k.lds_dyn) != hipSuccess)
         return MONOMOE_ERR_HIP;
-    if (o < 1) return MONOMOE_ERR_OCCUPANCY;
+    if (residency(o, pl->num_cus, pl->num_cus) != MONOMOE_OK) return MONOMOE_ERR_OCCUPANCY;
     k.occupancy = o;
     *c = k;
     return MONOMOE_OK;
@@ -647,6 +670,26 @@ int monomoe_plan_reset(monomoe_plan_t plan) {
     if (!plan) return MONOMOE_ERR_INVALID;
     if (hipDeviceSynchronize() != hipSuccess) return MONOMOE_ERR_HIP;
     return zero_workspace(plan);
+}
+
+int monomoe_layout(const monomoe_shape_t* shape, int topk, int kernel, int lds_total, int lds_static,
+                   int occupancy, int grid, int num_cus, monomoe_layout_t* out) {
+    if (!shape || !out) return MONOMOE_ERR_INVALID;
+    const monomoe_shape_t s = *shape;
+    const int sc = check_shape(s, topk);
+    if (sc != MONOMOE_OK) return sc;
+    if (kernel != MONOMOE_KERNEL_SINGLE && kernel != MONOMOE_KERNEL_MULTI) return MONOMOE_ERR_INVALID;
+    if (lds_static < 0 || lds_total <= lds_static || occupancy < 0 || grid < 0 || num_cus < 1) return MONOMOE_ERR_INVALID;
+    KernelConfig k{};
+    const int lr = kernel == MONOMOE_KERNEL_SINGLE ? single_layout(s.H, s.I, s.T, lds_total - lds_static, &k)
+                                                   : multi_layout(s.H, s.I, s.T, s.E, topk, 0, lds_total - lds_static, &k);
+    if (lr != MONOMOE_OK) return lr;
+    out->tokens_per_pass = k.tchunk;
+    out->group_tokens = kernel == MONOMOE_KERNEL_MULTI ? k.rows : 0;
+    out->act_buffers = k.naq;
+    out->handoff_slots = k.nslots;
+    out->lds_bytes = k.lds_dyn;
+    return residency(occupancy, grid == 0 ? num_cus : grid, num_cus);
 }
 
 int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info) {

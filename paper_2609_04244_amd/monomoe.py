@@ -27,7 +27,7 @@ KERNEL_MULTI = 2
 # Every symbol include/monomoe.h declares.
 EXPORTS = (
     "monomoe_plan", "monomoe_plan_destroy", "monomoe_plan_set_router_bias", "monomoe_plan_set_routing",
-    "monomoe_plan_set_schedule",
+    "monomoe_plan_set_schedule", "monomoe_layout",
     "monomoe_forward", "monomoe_forward_tokens", "monomoe_forward_noalloc",
     "monomoe_forward_debug", "monomoe_forward_timed", "monomoe_plan_status", "monomoe_plan_reset", "monomoe_plan_info",
     "monomoe_supported_shape", "monomoe_status_string", "monomoe_stream_copy", "monomoe_stream_read",
@@ -65,6 +65,11 @@ class Schedule(ctypes.Structure):
                 ("group_tokens", ctypes.c_int32), ("general_only", ctypes.c_int32)]
 
 
+class Layout(ctypes.Structure):
+    _fields_ = [("tokens_per_pass", ctypes.c_int32), ("group_tokens", ctypes.c_int32),
+                ("act_buffers", ctypes.c_int32), ("handoff_slots", ctypes.c_int32), ("lds_bytes", ctypes.c_int32)]
+
+
 _lib = None
 
 
@@ -86,6 +91,8 @@ def lib():
         L.monomoe_plan_set_routing.restype = ctypes.c_int
         L.monomoe_plan_set_schedule.argtypes = [vp, ctypes.POINTER(Schedule)]
         L.monomoe_plan_set_schedule.restype = ctypes.c_int
+        L.monomoe_layout.argtypes = [ctypes.POINTER(Shape)] + [ctypes.c_int] * 7 + [ctypes.POINTER(Layout)]
+        L.monomoe_layout.restype = ctypes.c_int
         L.monomoe_forward.argtypes = [vp] * 9
         L.monomoe_forward.restype = ctypes.c_int
         L.monomoe_forward_tokens.argtypes = [vp, ctypes.c_int32] + [vp] * 8
@@ -116,6 +123,15 @@ def lib():
 
 def status_string(code):
     return lib().monomoe_status_string(int(code)).decode()
+
+
+def layout(T, H, E, I, topk, kernel, lds_total, lds_static, occupancy, grid=0, num_cus=256):
+    """monomoe_layout (host arithmetic, no device): (status code, layout dict or None)."""
+    out = Layout()
+    rc = lib().monomoe_layout(ctypes.byref(Shape(T, H, E, I)), topk, kernel, lds_total, lds_static, occupancy,
+                              grid, num_cus, ctypes.byref(out))
+    fields = {f: getattr(out, f) for f, _ in Layout._fields_}
+    return rc, (fields if rc in (MONOMOE_OK, MONOMOE_ERR_OCCUPANCY) else None)
 
 
 def supported_shape(H, I):

@@ -75,6 +75,7 @@ def test_null_arguments():
     assert L.monomoe_plan_status(None) == mm.MONOMOE_ERR_INVALID
     assert L.monomoe_plan_reset(None) == mm.MONOMOE_ERR_INVALID
     assert L.monomoe_plan_info(None, None) == mm.MONOMOE_ERR_INVALID
+    assert L.monomoe_layout(None, 8, 1, 163840, 8192, 1, 0, 256, None) == mm.MONOMOE_ERR_INVALID
     L.monomoe_plan_destroy(None)
 
 
@@ -84,7 +85,7 @@ def test_binding_structs_match_the_header_layout(tmp_path):
     if not os.path.isfile("/opt/rocm/include/hip/hip_runtime_api.h"):
         pytest.skip("HIP headers not installed")
     structs = [("monomoe_shape_t", mm.Shape), ("monomoe_debug_t", mm.Debug), ("monomoe_plan_info_t", mm.PlanInfo),
-               ("monomoe_schedule_t", mm.Schedule)]
+               ("monomoe_schedule_t", mm.Schedule), ("monomoe_layout_t", mm.Layout)]
     lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "monomoe.h"', "int main(void) {"]
     for cname, py in structs:
         lines.append('printf("%s %%zu\\n", sizeof(%s));' % (cname, cname))
