@@ -169,7 +169,10 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
         f_xq = 0;
     }
     if (tid < kSlotsMax) f_cnt[tid] = 0;
-    for (int e = tid; e < E; e += kThreads) emask[e] = 0u;   // ordered by the barrier after top-k
+    for (int e = tid; e < E; e += kThreads) emask[e] = 0u;
+    // the flags are set before any wavefront uses them (workgroups without router rows have
+    // no other barrier before their first flag accesses)
+    __syncthreads();
     if (tid == 0) stamp(p.stamps, wg, kStEntry);
 
     // ---------------- stage 0: router slice + input quantisation slice ----------------
