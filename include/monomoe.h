@@ -176,7 +176,15 @@ int monomoe_forward_noalloc(const monomoe_shape_t* shape, int topk, int renorm, 
  *   fail_flag                     nonzero makes every workgroup wait on a condition that
  *                                 never holds (bounded by the spin limit), so the kernel
  *                                 takes its timeout path and reports MONOMOE_ERR_TIMEOUT
- *                                 through monomoe_plan_status(). */
+ *                                 through monomoe_plan_status().
+ *   jitter_seed                   race perturbation: nonzero (at most 65535) inserts
+ *                                 pseudo-random pauses of 0 to 2.55 us, a function of the
+ *                                 seed, at every cross-wavefront and cross-workgroup
+ *                                 hand-off point (partial sums, activation and contribution
+ *                                 stores, activation polls, output reduction, kernel
+ *                                 entry), so the readiness protocol runs under orders of
+ *                                 arrival it rarely sees; results must not change.  0: off.
+ *                                 MONOMOE_ERR_INVALID above 65535. */
 typedef struct {
     int32_t* topk_ids;
     float* topk_w;
@@ -191,6 +199,7 @@ typedef struct {
     uint64_t* stamps;
     uint64_t spin_limit_ticks;
     int32_t fail_flag;
+    uint32_t jitter_seed;
 } monomoe_debug_t;
 
 int monomoe_forward_debug(monomoe_plan_t plan, const void* x, const void* router_w,

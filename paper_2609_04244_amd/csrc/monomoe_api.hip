@@ -337,6 +337,10 @@ int launch(monomoe_plan_t plan, int T, const void* x, const void* router_w, cons
         if ((dbg->xq == nullptr) != (dbg->xs == nullptr)) return MONOMOE_ERR_INVALID;
         if ((dbg->aq == nullptr) != (dbg->as == nullptr)) return MONOMOE_ERR_INVALID;
         if ((dbg->topk_ids_in == nullptr) != (dbg->topk_w_in == nullptr)) return MONOMOE_ERR_INVALID;
+        if (dbg->jitter_seed > 0xFFFFu) return MONOMOE_ERR_INVALID;
+#ifndef MONOMOE_RACE_PERTURB
+        if (dbg->jitter_seed != 0) return MONOMOE_ERR_UNSUPPORTED;   // the perturbation build's hook
+#endif
         p.d_ids = dbg->topk_ids;
         p.d_w = dbg->topk_w;
         p.d_xq = dbg->xq;
@@ -349,7 +353,8 @@ int launch(monomoe_plan_t plan, int T, const void* x, const void* router_w, cons
         p.inj_w = dbg->topk_w_in;
         p.stamps = dbg->stamps;
         if (dbg->spin_limit_ticks) p.spin_limit = dbg->spin_limit_ticks;
-        p.fail_flag = dbg->fail_flag;
+        p.fail_flag = dbg->fail_flag != 0;
+        p.jitter = (uint16_t)dbg->jitter_seed;
     }
     p.E = s.E;
     p.k = plan->topk;

@@ -77,6 +77,33 @@ __device__ __forceinline__ void stamp(uint64_t* stamps, int wg, int which) {
     if (stamps) stamps[wg * kStamps + which] = now();
 }
 
+// Race perturbation (compiled into the perturbation build of the library only, which defines
+// MONOMOE_RACE_PERTURB): a pseudo-random pause of 0 to 2.55 us (s_memrealtime ticks of 10 ns)
+// at a hand-off point, taken at about half of the calls; seed 0 returns at once.  The pause
+// depends only on (seed, workgroup, wavefront, site, n), all uniform across the wavefront,
+// mixed by the lowbias32 integer hash (C. Wellons, "hash prospector"), so a seed replays the
+// same perturbation.  In the product build MONOMOE_PERTURB is empty: its kernels carry no
+// trace of the hook.
+__device__ __forceinline__ void jitter(uint32_t seed, int wg, int wv, int site, int n) {
+    if (seed == 0u) return;
+    uint32_t h = seed * 0x9E3779B9u ^ (uint32_t)wg * 0x85EBCA6Bu ^ ((uint32_t)wv << 24) ^ ((uint32_t)site << 20) ^
+                 (uint32_t)n;
+    h ^= h >> 16;
+    h *= 0x7FEB352Du;
+    h ^= h >> 15;
+    h *= 0x846CA68Bu;
+    h ^= h >> 16;
+    if (h & 1u) return;
+    const uint64_t d = (h >> 8) & 255u;
+    const uint64_t t0 = now();
+    while (now() - t0 < d) __builtin_amdgcn_s_sleep(1);
+}
+#ifdef MONOMOE_RACE_PERTURB
+#define MONOMOE_PERTURB(site, n) jitter(p.jitter, wg, wv, (site), (n))
+#else
+#define MONOMOE_PERTURB(site, n) ((void)0)
+#endif
+
 // Record the first device-side error; later ones keep the first code.
 __device__ __forceinline__ void set_status(uint32_t* status, uint32_t code) {
     uint32_t expected = kDevOk;

@@ -174,6 +174,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
     // no other barrier before their first flag accesses)
     __syncthreads();
     if (tid == 0) stamp(p.stamps, wg, kStEntry);
+    MONOMOE_PERTURB(0, 0);
 
     // ---------------- stage 0: router slice + input quantisation slice ----------------
     if (ONE || T == 1) router_rows<H, 1>(p, wg, G, tid, tag, red);
@@ -504,6 +505,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
         auto handoff = [&](const v4f& acc) -> bool {   // partial sums of unit cm to the helper
             const int useq = (cph == 0) ? cm : (nu + cm);
             const int slot = useq & smask;
+            MONOMOE_PERTURB(1, useq);
             if (!wait_lds(&f_consumed, useq - smask, &f_abort, limit)) return false;
             part[(slot * NC + wv) * 64 + lane] = acc;
             if (lane == 0) lds_add(&f_cnt[slot], 1);
@@ -611,6 +613,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
             }
             lds_st(&f_cnt[slot], 0);
             lds_st(&f_consumed, j + 1);
+            MONOMOE_PERTURB(2, j);
             const int c = lane & 15;
             if (lane < 32 && c < T && ((tmask >> c) & 1u)) {
                 v4f a;
@@ -728,6 +731,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
             const int m = dlo + j, u = m / DNE, ht = m - u * DNE, x = u - dn_u0;
             const int useq = nu + j, slot = useq & smask;
             while (prepared <= x) {
+                MONOMOE_PERTURB(3, prepared);
                 if (!prepare(prepared, true)) { fine = false; break; }
                 if (prepared == 0 && lane == 0) stamp(p.stamps, wg, kStFirstAq);
                 prepared += 1;
@@ -742,6 +746,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
             for (int b = 0; b < NCD; ++b) y += part[(slot * NC + ((IP >= NC) ? b : (j % NC))) * 64 + lane];
             lds_st(&f_cnt[slot], 0);
             lds_st(&f_consumed, useq + 1);
+            MONOMOE_PERTURB(4, j);
             const uint32_t tmask = act_m[u];
             const int c = lane & 15;
             if (c < T && ((tmask >> c) & 1u)) {   // this token's weighted contribution, tagged
@@ -770,6 +775,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
         const int nchunk = (H / 16) * ((T + 3) / 4);
         for (int r = wg + G * wv; r < nchunk; r += G * kWaves) {
             const int c = r / (H / 16), ht = r - c * (H / 16);
+            MONOMOE_PERTURB(5, r);
             if (!reduce_chunk<H>(p, ht, 64 * c, T, K, tag, lane, status, limit)) break;
         }
     }

@@ -89,7 +89,8 @@ struct KParams {
     const float* inj_w;
     uint64_t* stamps;         // [grid][kStamps]
     uint64_t spin_limit;      // 100 MHz ticks
-    int32_t fail_flag;
+    int16_t fail_flag;
+    uint16_t jitter;          // race-perturbation seed (0: off)
     // runtime shape and LDS layout
     int32_t T, E, k, renorm;
     int32_t policy;           // MONOMOE_ROUTING_SOFTMAX / MONOMOE_ROUTING_SIGMOID_BIAS

@@ -11,6 +11,9 @@ import torch  # loads torch's HIP runtime first, so the library binds to the sam
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmonomoe.so")
+# the race-perturbation build: the same sources with a pseudo-random pause at every hand-off
+# point, taken when monomoe_forward_debug's jitter_seed is nonzero (test use only)
+LIB_PERTURB_PATH = os.path.join(_HERE, "libmonomoe_perturb.so")
 
 MONOMOE_OK = 0
 MONOMOE_ERR_INVALID = -1
@@ -50,6 +53,7 @@ class Debug(ctypes.Structure):
         ("xs", ctypes.c_void_p), ("act", ctypes.c_void_p), ("aq", ctypes.c_void_p), ("as_", ctypes.c_void_p),
         ("out_f32", ctypes.c_void_p), ("topk_ids_in", ctypes.c_void_p), ("topk_w_in", ctypes.c_void_p),
         ("stamps", ctypes.c_void_p), ("spin_limit_ticks", ctypes.c_uint64), ("fail_flag", ctypes.c_int32),
+        ("jitter_seed", ctypes.c_uint32),
     ]
 
 
@@ -70,16 +74,25 @@ class Layout(ctypes.Structure):
                 ("act_buffers", ctypes.c_int32), ("handoff_slots", ctypes.c_int32), ("lds_bytes", ctypes.c_int32)]
 
 
-_lib = None
+_libs = {}
 
 
 def lib():
     """Load libmonomoe.so (built by __graft_entry__.build()); raise if it is missing."""
-    global _lib
-    if _lib is None:
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError("libmonomoe.so is not built (%s); run __graft_entry__.build()" % LIB_PATH)
-        L = ctypes.CDLL(LIB_PATH)
+    return _load(LIB_PATH)
+
+
+def lib_perturb():
+    """Load libmonomoe_perturb.so, the race-perturbation build (test use only)."""
+    return _load(LIB_PERTURB_PATH)
+
+
+def _load(path):
+    if path not in _libs:
+        if not os.path.exists(path):
+            raise RuntimeError("%s is not built; run __graft_entry__.build()" % path)
+        # RTLD_LOCAL (ctypes' default): both builds can be loaded side by side
+        L = ctypes.CDLL(path, mode=os.RTLD_LOCAL)
         vp = ctypes.c_void_p
         L.monomoe_plan.argtypes = [ctypes.POINTER(Shape), ctypes.c_int, ctypes.c_int, ctypes.POINTER(vp)]
         L.monomoe_plan.restype = ctypes.c_int
@@ -117,8 +130,8 @@ def lib():
         L.monomoe_stream_copy.restype = ctypes.c_int
         L.monomoe_stream_read.argtypes = [vp, ctypes.c_size_t, vp, vp]
         L.monomoe_stream_read.restype = ctypes.c_int
-        _lib = L
-    return _lib
+        _libs[path] = L
+    return _libs[path]
 
 
 def status_string(code):
@@ -231,18 +244,21 @@ def _stream(stream):
 class Plan:
     """A plan for one shape (T, H, E, I) with top-k and renormalisation fixed."""
 
-    def __init__(self, T, H, E, I, topk, renorm=True):
+    def __init__(self, T, H, E, I, topk, renorm=True, perturb=False):
+        """perturb: make the plan with the race-perturbation build of the library (its
+        launches pause at hand-off points when forward_debug gets a nonzero jitter_seed)."""
         self.T, self.H, self.E, self.I, self.topk, self.renorm = int(T), int(H), int(E), int(I), int(topk), bool(renorm)
+        self._L = lib_perturb() if perturb else lib()
         self._h = ctypes.c_void_p()
         self._bias = None
-        rc = lib().monomoe_plan(ctypes.byref(Shape(self.T, self.H, self.E, self.I)), self.topk, int(self.renorm),
+        rc = self._L.monomoe_plan(ctypes.byref(Shape(self.T, self.H, self.E, self.I)), self.topk, int(self.renorm),
                                 ctypes.byref(self._h))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_plan")
 
     def close(self):
         if self._h:
-            lib().monomoe_plan_destroy(self._h)
+            self._L.monomoe_plan_destroy(self._h)
             self._h = ctypes.c_void_p()
 
     def __del__(self):
@@ -259,14 +275,14 @@ class Plan:
 
     def set_router_bias(self, bias):
         self._bias = bias  # keep the tensor alive while the plan refers to it
-        rc = lib().monomoe_plan_set_router_bias(self._h, _ptr(bias))
+        rc = self._L.monomoe_plan_set_router_bias(self._h, _ptr(bias))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_plan_set_router_bias")
 
     def set_routing(self, policy, sel_bias=None, scale=1.0):
         """ROUTING_SOFTMAX, or ROUTING_SIGMOID_BIAS with an fp32 [E] selection bias (or None)
         and the routed scaling factor."""
-        rc = lib().monomoe_plan_set_routing(self._h, int(policy), _ptr(sel_bias), float(scale))
+        rc = self._L.monomoe_plan_set_routing(self._h, int(policy), _ptr(sel_bias), float(scale))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_plan_set_routing")
         self._sel_bias = sel_bias  # keep the tensor alive while the plan refers to it
@@ -277,13 +293,13 @@ class Plan:
         general_only (1: passes of one token on the general single-tile kernel, not its
         one-token specialisation)."""
         sch = Schedule(int(grid), int(ring), int(kernel), int(group_tokens), int(general_only))
-        rc = lib().monomoe_plan_set_schedule(self._h, ctypes.byref(sch))
+        rc = self._L.monomoe_plan_set_schedule(self._h, ctypes.byref(sch))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_plan_set_schedule")
 
     def info(self):
         inf = PlanInfo()
-        rc = lib().monomoe_plan_info(self._h, ctypes.byref(inf))
+        rc = self._L.monomoe_plan_info(self._h, ctypes.byref(inf))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_plan_info")
         return {f: getattr(inf, f) for f, _ in PlanInfo._fields_}
@@ -307,7 +323,7 @@ class Plan:
             out = torch.empty((self.T, self.H), dtype=torch.bfloat16, device=x.device)
         if check:
             self._check(x, router_w, w13, w13_scale, w2, w2_scale, out)
-        rc = lib().monomoe_forward(self._h, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale), _ptr(w2),
+        rc = self._L.monomoe_forward(self._h, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale), _ptr(w2),
                                    _ptr(w2_scale), _ptr(out), _stream(stream))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_forward")
@@ -328,7 +344,7 @@ class Plan:
                 self._check(x, router_w, w13, w13_scale, w2, w2_scale, out)
             finally:
                 self.T = saved
-        rc = lib().monomoe_forward_tokens(self._h, T, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale),
+        rc = self._L.monomoe_forward_tokens(self._h, T, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale),
                                           _ptr(w2), _ptr(w2_scale), _ptr(out), _stream(stream))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_forward_tokens")
@@ -336,15 +352,16 @@ class Plan:
 
     def forward_timed(self, x, router_w, w13, w13_scale, w2, w2_scale, out, timer, stream=None):
         """monomoe_forward whose dispatch stamps `timer` (a DispatchTimer) with its own begin/end."""
-        rc = lib().monomoe_forward_timed(self._h, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale), _ptr(w2),
+        rc = self._L.monomoe_forward_timed(self._h, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale), _ptr(w2),
                                          _ptr(w2_scale), _ptr(out), timer.start, timer.stop, _stream(stream))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_forward_timed")
         return out
 
     def forward_debug(self, x, router_w, w13, w13_scale, w2, w2_scale, out=None, ids_in=None, w_in=None,
-                      spin_limit_ticks=0, fail_flag=False, stream=None):
-        """Forward with every test hook enabled; returns (out, dict of device tensors)."""
+                      spin_limit_ticks=0, fail_flag=False, jitter_seed=0, stream=None):
+        """Forward with every test hook enabled; returns (out, dict of device tensors).
+        `jitter_seed` nonzero (<= 65535) perturbs the hand-off timing (race perturbation)."""
         T, H, I, k = self.T, self.H, self.I, self.topk
         dev = x.device
         if out is None:
@@ -370,8 +387,8 @@ class Plan:
                     d["act"].data_ptr(), d["aq"].data_ptr(), d["as"].data_ptr(), d["out_f32"].data_ptr(),
                     ids_in.data_ptr() if ids_in is not None else None,
                     w_in.data_ptr() if w_in is not None else None,
-                    d["stamps"].data_ptr(), int(spin_limit_ticks), int(bool(fail_flag)))
-        rc = lib().monomoe_forward_debug(self._h, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale), _ptr(w2),
+                    d["stamps"].data_ptr(), int(spin_limit_ticks), int(bool(fail_flag)), int(jitter_seed))
+        rc = self._L.monomoe_forward_debug(self._h, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale), _ptr(w2),
                                          _ptr(w2_scale), _ptr(out), ctypes.byref(dbg), _stream(stream))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_forward_debug")
@@ -381,17 +398,17 @@ class Plan:
     def forward_stamped(self, x, router_w, w13, w13_scale, w2, w2_scale, out, stamps, stream=None):
         """Forward with only the phase-stamp hook enabled: `stamps` is an int64 device tensor
         [grid, 24] that receives each workgroup's s_memrealtime (100 MHz) stamps."""
-        dbg = Debug(None, None, None, None, None, None, None, None, None, None, stamps.data_ptr(), 0, 0)
-        rc = lib().monomoe_forward_debug(self._h, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale), _ptr(w2),
+        dbg = Debug(None, None, None, None, None, None, None, None, None, None, stamps.data_ptr(), 0, 0, 0)
+        rc = self._L.monomoe_forward_debug(self._h, _ptr(x), _ptr(router_w), _ptr(w13), _ptr(w13_scale), _ptr(w2),
                                          _ptr(w2_scale), _ptr(out), ctypes.byref(dbg), _stream(stream))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_forward_debug")
         return out
 
     def status(self):
-        return lib().monomoe_plan_status(self._h)
+        return self._L.monomoe_plan_status(self._h)
 
     def reset(self):
-        rc = lib().monomoe_plan_reset(self._h)
+        rc = self._L.monomoe_plan_reset(self._h)
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_plan_reset")

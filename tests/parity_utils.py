@@ -114,11 +114,12 @@ def exact_tie_tokens(logits, k):
     return s[:, k - 1] == s[:, k]
 
 
-def run_case(inp, tokens=None, plan=None, exact_ties=False, min_near_ties=0):
+def run_case(inp, tokens=None, plan=None, exact_ties=False, min_near_ties=0, jitter_seed=0):
     """Run the GPU operator on `inp` (device tensors from workloads.generate) and compare
     with the oracle on `tokens` (default: all; the oracle's rows are independent per
     token).  exact_ties: also compare the ids of tokens whose boundary scores tie exactly.
-    min_near_ties: the case must contain at least this many near-tie tokens.  Returns a
+    min_near_ties: the case must contain at least this many near-tie tokens.  jitter_seed:
+    run the GPU launches under the race-perturbation test hook with this seed.  Returns a
     report dict; raises AssertionError on a contract violation."""
     T, H, E, I, k, renorm = inp["T"], inp["H"], inp["E"], inp["I"], inp["k"], inp["renorm"]
     own = plan is None
@@ -132,7 +133,7 @@ def run_case(inp, tokens=None, plan=None, exact_ties=False, min_near_ties=0):
     tie = near_tie_tokens(logits, k)
     assert int(tie.sum()) >= min_near_ties, "expected at least %d near-tie tokens, got %d" % (min_near_ties, tie.sum())
     exact = exact_tie_tokens(logits, k) if exact_ties else np.zeros(T, bool)
-    g = _gpu(plan, inp)
+    g = _gpu(plan, inp, jitter_seed=jitter_seed)
     # 1. routing: ids bit-exact as sets and weights close, except near-tie tokens (tokens
     #    with an exact tie have one correct answer and are compared when asked)
     for t in range(T):
@@ -146,7 +147,8 @@ def run_case(inp, tokens=None, plan=None, exact_ties=False, min_near_ties=0):
     unique = int(len(set(g["ids"].reshape(-1).tolist())))
     if tie.any():
         # the oracle's selection is injected for the rest of the comparison
-        g = _gpu(plan, inp, ids_in=torch.from_numpy(oids), w_in=torch.from_numpy(ow.astype(np.float32)))
+        g = _gpu(plan, inp, ids_in=torch.from_numpy(oids), w_in=torch.from_numpy(ow.astype(np.float32)),
+                 jitter_seed=jitter_seed)
     if own:
         plan.close()
 

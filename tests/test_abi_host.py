@@ -21,8 +21,9 @@ def test_header_declares_the_binding_exports():
     assert declared_functions() == sorted(mm.EXPORTS)
 
 
-def test_library_loads_and_exports_every_declared_symbol():
-    L = mm.lib()
+@pytest.mark.parametrize("which", ["product", "perturbation"])
+def test_library_loads_and_exports_every_declared_symbol(which):
+    L = mm.lib() if which == "product" else mm.lib_perturb()
     for name in declared_functions():
         assert hasattr(L, name), name
         assert ctypes.cast(getattr(L, name), ctypes.c_void_p).value
