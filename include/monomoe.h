@@ -302,6 +302,53 @@ typedef struct {
 int monomoe_layout(const monomoe_shape_t* shape, int topk, int kernel, int lds_total, int lds_static,
                    int occupancy, int grid, int num_cus, monomoe_layout_t* out);
 
+/* Host-side model check of the single-tile kernel's hand-off protocol (Sec. 3.2: readiness-
+ * based hand-offs between resident workgroups, no grid barrier), without a device.  For one
+ * routing, every wavefront's synchronisation events are replayed in the order the kernel
+ * issues them, with the kernel's own work-partition arithmetic: workgroup barriers, router
+ * rows, the input exchange, the selection (with one token: each top-k position published as
+ * it is ranked, and the compute wavefronts' quantisation counter), the partial-sum hand-off
+ * slots, the requantised-activation buffers (blocking and non-blocking preparation), the
+ * activation and contribution words, the output reduction.  A scheduler interleaves the
+ * wavefronts in a pseudo-random order drawn from `seed` (0: in index order, one event each)
+ * with at most `resident` workgroups resident at once, started in index order (a new one when
+ * one ends).  The result says whether every wavefront ran to its end (no deadlock) and counts
+ * safety violations: a hand-off slot rewritten before the helper consumed it, a slot
+ * consumed that does not hold the expected sums, an activation buffer read while it holds
+ * another expert or rewritten while it is read, a unit published twice.  A unit that no
+ * workgroup owns shows as a deadlock (its consumers wait forever).
+ *   shape, topk      as for monomoe_plan; shape->T <= 16 (one pass)
+ *   topk_ids         host int32 [T, topk]: the selection to replay, ids in [0, E), distinct
+ *                    per token (the order within a token is its top-k order)
+ *   one_token        1: the one-token specialisation (T must be 1); 0: the general kernel
+ *   grid, ring       persistent workgroups (<= 1024) and weight-ring depth (2 or 4)
+ *   handoff_slots, act_buffers   the LDS layout (monomoe_layout: a power of two <= 32; 1 or 2)
+ *   mutate           0 for the kernel's protocol; MONOMOE_SCHEDULE_MUTATE_* bits remove a
+ *                    wait or move a step, so that a test can show the check catches the
+ *                    resulting race
+ * Returns MONOMOE_ERR_INVALID for bad arguments, MONOMOE_ERR_UNSUPPORTED beyond one pass,
+ * else fills *out and returns MONOMOE_OK (whatever the verdict). */
+#define MONOMOE_SCHEDULE_MUTATE_NO_SLOT_WAIT 1u    /* hand off without waiting for a free slot        */
+#define MONOMOE_SCHEDULE_MUTATE_NO_ACT_WAIT 2u     /* read an activation buffer without waiting       */
+#define MONOMOE_SCHEDULE_MUTATE_PREFETCH_ONE_BUFFER 4u  /* prefetch the next expert with one buffer */
+typedef struct {
+    int32_t complete;        /* 1: every wavefront of every workgroup ran to its end          */
+    int32_t violations;      /* safety violations seen (0 for a sound protocol)               */
+    int32_t first_violation; /* kind of the first: 1 slot overwritten, 2 stale slot consumed,
+                                3 buffer read holding another expert, 4 buffer overwritten
+                                while read, 5 a unit published twice; 0 none                  */
+    int32_t active_experts;  /* expert slots of the routing                                   */
+    int64_t events;          /* synchronisation events executed                               */
+    int32_t blocked_wg;      /* at a deadlock: a blocked wavefront's workgroup, wavefront    */
+    int32_t blocked_wave;    /*   (helper = 4) and its event kind; -1 when complete          */
+    int32_t blocked_event;
+    int32_t reserved;
+} monomoe_schedule_report_t;
+
+int monomoe_schedule_check(const monomoe_shape_t* shape, int topk, const int32_t* topk_ids, int one_token,
+                           int grid, int ring, int handoff_slots, int act_buffers, int resident, uint32_t seed,
+                           uint32_t mutate, monomoe_schedule_report_t* out);
+
 /* 1 if (H, I) is one of the compiled shapes, else 0. */
 int monomoe_supported_shape(int32_t H, int32_t I);
 

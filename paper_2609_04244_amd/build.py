@@ -21,7 +21,7 @@ BUILD_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libmonomoe.so")
 LIB_PERTURB = os.path.join(HERE, "libmonomoe_perturb.so")
 SOURCES = ["monomoe_kernel.hip", "monomoe_kernel_one.hip", "monomoe_kernel_mt.hip", "monomoe_api.hip",
-           "monomoe_stream.hip"]
+           "monomoe_stream.hip", "monomoe_schedule.hip"]
 ARCH = "gfx950"
 LIBRARIES = {LIB: [], LIB_PERTURB: ["-DMONOMOE_RACE_PERTURB"]}   # library -> extra defines
 

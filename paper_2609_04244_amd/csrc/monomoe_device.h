@@ -5,6 +5,7 @@
 #pragma once
 
 #include "monomoe_internal.h"
+#include "monomoe_partition.h"
 
 namespace monomoe {
 
@@ -348,13 +349,12 @@ __device__ __forceinline__ void quantise_input(const uint16_t* __restrict__ x, i
 // the 128-groups are split over the workgroups; each quantises its share once (the same
 // arithmetic as quantise_loaded) and publishes the codes as tagged words {4 codes, tag}
 // and the scales as {fp32, tag}; every workgroup then polls all of them into its LDS.
-constexpr int kLocalQuantChunks = 16;
 template <int H>
 __device__ __forceinline__ void publish_input_groups(const KParams& p, int T, int wg, int G, int tid, uint32_t tag) {
     constexpr int HB = H / 128, GPP = kThreads / 16;   // groups per pass: one per DPP row
     const int NG = T * HB;
-    const int q0 = (int)((uint32_t)wg * (uint32_t)NG / (uint32_t)G);
-    const int q1 = (int)((uint32_t)(wg + 1) * (uint32_t)NG / (uint32_t)G);
+    const int q0 = range_lo(wg, G, NG);
+    const int q1 = range_lo(wg + 1, G, NG);
     const uint64_t tag_hi = (uint64_t)tag << 32;
     const int r = tid & 15;
     for (int qb = q0; qb < q1; qb += GPP) {

@@ -327,9 +327,9 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
     const int n_up = U * UPE, n_dn = U * DNE;
     static_assert((uint64_t)kUMax * (H / 16) * kGridMax < (1ull << 32) &&
                       (uint64_t)kUMax * (I / 8) + kGridMax < (1ull << 31), "partition arithmetic");
-    const int nu = n_up > wg ? (n_up - 1 - wg) / G + 1 : 0;   // gate/up units of this workgroup
-    const int dlo = (int)((uint32_t)wg * (uint32_t)n_dn / (uint32_t)G);
-    const int dhi = (int)((uint32_t)(wg + 1) * (uint32_t)n_dn / (uint32_t)G);
+    const int nu = up_count(wg, G, n_up);                     // gate/up units of this workgroup
+    const int dlo = range_lo(wg, G, n_dn);
+    const int dhi = range_lo(wg + 1, G, n_dn);
     const int nd = dhi - dlo;                                 // down units of this workgroup
     const int dn_u0 = nd > 0 ? dlo / DNE : 0;                 // first expert slot of the down range
 
@@ -416,7 +416,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
         auto lbase = [&]() MONOMOE_CURSOR_INLINE {   // per-lane addresses of task lkp of unit lm
             const int kb = 2 * lkp;
             if (lph == 0) {
-                const int mu = wg + G * lm;   // the unit
+                const int mu = up_unit(wg, G, lm);   // the unit
                 const int u = mu / UPE, i0 = (mu - u * UPE) * 8;
                 if constexpr (ONE) ranked(u);
                 const int e = ONE ? min(max(uni(sel_ids[u]), 0), E - 1) : uni(act_e[u]);
@@ -598,7 +598,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
 
         // --- gate/up epilogues: SiLU(gate)*up, stored as tagged words ---
         for (int j = 0; j < nu; ++j) {
-            const int m = wg + G * j, slot = j & smask;
+            const int m = up_unit(wg, G, j), slot = j & smask;
             if (!wait_lds(&f_cnt[slot], NCU, &f_abort, limit)) { fine = false; break; }
             const int u = m / UPE, i0 = (m - u * UPE) * 8;
             const uint32_t tmask = act_m[u];

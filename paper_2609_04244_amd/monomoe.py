@@ -30,7 +30,7 @@ KERNEL_MULTI = 2
 # Every symbol include/monomoe.h declares.
 EXPORTS = (
     "monomoe_plan", "monomoe_plan_destroy", "monomoe_plan_set_router_bias", "monomoe_plan_set_routing",
-    "monomoe_plan_set_schedule", "monomoe_layout",
+    "monomoe_plan_set_schedule", "monomoe_layout", "monomoe_schedule_check",
     "monomoe_forward", "monomoe_forward_tokens", "monomoe_forward_noalloc",
     "monomoe_forward_debug", "monomoe_forward_timed", "monomoe_plan_status", "monomoe_plan_reset", "monomoe_plan_info",
     "monomoe_supported_shape", "monomoe_status_string", "monomoe_stream_copy", "monomoe_stream_read",
@@ -67,6 +67,17 @@ class PlanInfo(ctypes.Structure):
 class Schedule(ctypes.Structure):
     _fields_ = [("grid", ctypes.c_int32), ("ring", ctypes.c_int32), ("kernel", ctypes.c_int32),
                 ("group_tokens", ctypes.c_int32), ("general_only", ctypes.c_int32)]
+
+
+class ScheduleReport(ctypes.Structure):
+    _fields_ = [("complete", ctypes.c_int32), ("violations", ctypes.c_int32), ("first_violation", ctypes.c_int32),
+                ("active_experts", ctypes.c_int32), ("events", ctypes.c_int64), ("blocked_wg", ctypes.c_int32),
+                ("blocked_wave", ctypes.c_int32), ("blocked_event", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+SCHEDULE_MUTATE_NO_SLOT_WAIT = 1
+SCHEDULE_MUTATE_NO_ACT_WAIT = 2
+SCHEDULE_MUTATE_PREFETCH_ONE_BUFFER = 4
 
 
 class Layout(ctypes.Structure):
@@ -106,6 +117,9 @@ def _load(path):
         L.monomoe_plan_set_schedule.restype = ctypes.c_int
         L.monomoe_layout.argtypes = [ctypes.POINTER(Shape)] + [ctypes.c_int] * 7 + [ctypes.POINTER(Layout)]
         L.monomoe_layout.restype = ctypes.c_int
+        L.monomoe_schedule_check.argtypes = [ctypes.POINTER(Shape), ctypes.c_int, vp] + [ctypes.c_int] * 6 + \
+            [ctypes.c_uint32, ctypes.c_uint32, ctypes.POINTER(ScheduleReport)]
+        L.monomoe_schedule_check.restype = ctypes.c_int
         L.monomoe_forward.argtypes = [vp] * 9
         L.monomoe_forward.restype = ctypes.c_int
         L.monomoe_forward_tokens.argtypes = [vp, ctypes.c_int32] + [vp] * 8
@@ -145,6 +159,21 @@ def layout(T, H, E, I, topk, kernel, lds_total, lds_static, occupancy, grid=0, n
                               grid, num_cus, ctypes.byref(out))
     fields = {f: getattr(out, f) for f, _ in Layout._fields_}
     return rc, (fields if rc in (MONOMOE_OK, MONOMOE_ERR_OCCUPANCY) else None)
+
+
+def schedule_check(ids, H, E, I, one_token, grid, ring, handoff_slots, act_buffers, resident=None, seed=0,
+                   mutate=0):
+    """monomoe_schedule_check (host model of the single-tile kernel's hand-offs, no device) for
+    the selection `ids` (int array [T, topk]): (status code, report dict or None)."""
+    import numpy as np
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    T, k = ids.shape
+    out = ScheduleReport()
+    rc = lib().monomoe_schedule_check(ctypes.byref(Shape(T, H, E, I)), k, ids.ctypes.data_as(ctypes.c_void_p),
+                                      int(one_token), int(grid), int(ring), int(handoff_slots), int(act_buffers),
+                                      int(grid if resident is None else resident), int(seed), int(mutate),
+                                      ctypes.byref(out))
+    return rc, ({f: getattr(out, f) for f, _ in ScheduleReport._fields_} if rc == MONOMOE_OK else None)
 
 
 def supported_shape(H, I):

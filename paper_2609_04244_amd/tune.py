@@ -10,7 +10,11 @@ For one workload and a list of token counts:
 
   1. enumerate the candidates (combinations the plan rejects are dropped: the multi-tile
      kernel has ring depth 2 only, grids must be resident);
-  2. validation gate, against the default schedule's output on the same inputs (the default
+  2. protocol gate, on the host: a single-tile candidate's hand-off protocol, with its grid,
+     ring depth and LDS layout, must run to completion without a safety violation under the
+     host model check (monomoe_schedule_check) for a seeded routing of every pass size, before
+     the candidate is launched;
+     validation gate, against the default schedule's output on the same inputs (the default
      is what the parity tests check against the fp64 oracle; the package itself does not use
      the oracle, and tests/test_gpu_tuned_schedules.py runs every tuned schedule against it),
      with the device status OK: a candidate that runs the same kernel must be bit-identical
@@ -78,6 +82,30 @@ def apply_tuned(plan, workload, T, path=TABLE):
 SCHEDULE_KEYS = ("kernel", "grid", "ring", "general_only", "group_tokens")
 TIE = 0.01   # a schedule replaces the default at T only when faster by more than this fraction
 KERNEL_NAMES = {mm.KERNEL_SINGLE: "single", mm.KERNEL_MULTI: "multi"}
+
+
+def model_verdict(plan, cfg, T, general_only, seed=0):
+    """The host model check of the plan's single-tile schedule at T tokens: None when every
+    pass size runs to completion without a safety violation (a seeded routing each), else the
+    reason."""
+    info = plan.info()
+    tpp = info["tokens_per_pass"]
+    # the plan's LDS layout: the largest that fits exactly its own dynamic LDS bytes
+    rc, lay = mm.layout(tpp, cfg["H"], cfg["E"], cfg["I"], cfg["k"], mm.KERNEL_SINGLE, info["lds_bytes"] + 8192,
+                        8192, 1, info["grid"])
+    if rc != mm.MONOMOE_OK:
+        return "layout: %s" % mm.status_string(rc)
+    rng = np.random.default_rng(seed)
+    for Tp in sorted({min(tpp, T)} | ({T % tpp} if T % tpp else set())):
+        ids = np.stack([rng.choice(cfg["E"], size=cfg["k"], replace=False) for _ in range(Tp)])
+        one = int(Tp == 1 and not general_only)
+        rc, r = mm.schedule_check(ids, cfg["H"], cfg["E"], cfg["I"], one, info["grid"], info["ring"],
+                                  lay["handoff_slots"], lay["act_buffers"], seed=seed + 1)
+        if rc != mm.MONOMOE_OK:
+            return "model check: %s" % mm.status_string(rc)
+        if not r["complete"] or r["violations"]:
+            return "protocol model at %d tokens per pass: %s" % (Tp, r)
+    return None
 
 
 def label(c):
@@ -165,6 +193,11 @@ def main(argv=None):
             except mm.MonoMoEError as e:
                 rejected[c] = "not accepted: %s" % e
                 continue
+            if c[0] == mm.KERNEL_SINGLE:
+                why = model_verdict(plan, cfg, T, c[3], seed=T)
+                if why is not None:
+                    rejected[c] = why
+                    continue
             o = run(plan, layers[0], T, out)
             torch.cuda.synchronize()
             if plan.status() != mm.MONOMOE_OK:

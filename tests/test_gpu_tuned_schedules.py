@@ -41,6 +41,8 @@ def test_tuned_schedule_matches_the_oracle(name, T):
     assert tune.apply_tuned(plan, name, T)
     sch = tune.tuned_schedule(name, T)
     log("case %s T=%d tuned schedule %s" % (name, T, sch))
+    if not plan.info()["multi_tile"]:   # the tuner's host gate, on the plan as configured
+        assert tune.model_verdict(plan, wl.config(name), T, sch["general_only"]) is None
     rep = run_case(inp, plan=plan, tokens=sorted({0, T - 1}))
     log("  -> %s" % rep)
     plan.close()
