@@ -49,6 +49,14 @@ enum Ev : int8_t {
     kEvEnd,
 };
 
+enum : int {   // violation kinds (monomoe_schedule_report_t.first_violation)
+    kVioSlotOverwrite = 1,   // a hand-off slot rewritten before the helper consumed it
+    kVioSlotStale = 2,       // the helper consumed a slot that does not hold the expected sums
+    kVioBufferRead = 3,      // a compute wavefront read an activation buffer holding another expert
+    kVioBufferOverwrite = 4, // an activation buffer rewritten while a compute wavefront reads it
+    kVioDuplicate = 5,       // a gate/up or down unit published twice (partition overlap)
+};
+
 struct Step {
     Ev ev;
     int a, b, c;
@@ -64,11 +72,11 @@ struct Wave {
 
 struct Group {
     int wg;
-    int nu = 0, dlo = 0, dhi = 0, dn_u0 = 0, nx = 0;
+    int nu = 0, dlo = 0, nd = 0, nx = 0;   // gate/up units; the contiguous down range, its slots
     std::vector<int> barrier;     // arrivals per barrier index
     int f_rank = 0, f_xq = 0, f_consumed = 0;
     int f_aq_seq[2] = {0, 0};
-    int content[2] = {-1, -1};    // expert index held by each activation buffer
+    int content[2] = {-1, -1};    // expert slot held by each activation buffer (-2: partly written)
     std::vector<int> f_cnt;       // per slot
     std::vector<int> part;        // [slot][wave]: sequence number last written (-1: none)
     Wave w[kWaves];
@@ -88,7 +96,6 @@ struct Model {
     std::vector<uint8_t> act;       // gate/up unit published
     std::vector<int> act_slot;      // units published per expert slot
     std::vector<uint8_t> contrib;   // down unit published
-    std::vector<int> dn_owner;      // workgroup of each down unit
     std::vector<Group> g;
     int64_t events = 0;
     int violations = 0, first_violation = 0;
@@ -121,7 +128,7 @@ void build_compute(Model& M, Group& gr, int wv) {
         const int c = share(wv, m, M.HP, kp);
         for (int i = 0; i < c; ++i) tasks.push_back({0, m});
     }
-    for (int m = 0; m < gr.dhi - gr.dlo; ++m) {
+    for (int m = 0; m < gr.nd; ++m) {
         int kp;
         const int c = share(wv, m, M.IP, kp);
         for (int i = 0; i < c; ++i) tasks.push_back({1, m});
@@ -142,7 +149,7 @@ void build_compute(Model& M, Group& gr, int wv) {
                 xq_ready = true;
             }
         } else {
-            P.push_back({kEvWaitAq, (gr.dlo + t.m) / M.DNE - gr.dn_u0, 0, 0});
+            P.push_back({kEvWaitAq, (gr.dlo + t.m) / M.DNE - gr.dlo / M.DNE, 0, (gr.dlo + t.m) / M.DNE});
         }
     };
     if (tasks.empty()) return;
@@ -156,8 +163,9 @@ void build_compute(Model& M, Group& gr, int wv) {
         if (last) {
             const Task& t = tasks[i];
             const int useq = t.ph == 0 ? t.m : gr.nu + t.m;
-            const int x = t.ph == 0 ? -1 : (gr.dlo + t.m) / M.DNE - gr.dn_u0;
-            P.push_back({kEvHandoff, useq, x, 0});
+            const int u = t.ph == 0 ? -1 : (gr.dlo + t.m) / M.DNE;
+            const int x = t.ph == 0 ? -1 : u - gr.dlo / M.DNE;
+            P.push_back({kEvHandoff, useq, x, u});
             if (i + 1 < tasks.size()) cbase(i + 1);
         }
     }
@@ -170,8 +178,8 @@ void build_helper(Model& M, Group& gr) {
         P.push_back({kEvConsume, j, M.NCU, v});
         P.push_back({kEvPublishAct, up_unit(gr.wg, M.G, j), 0, 0});
     }
-    for (int j = 0; j < gr.dhi - gr.dlo; ++j) {
-        const int x = (gr.dlo + j) / M.DNE - gr.dn_u0;
+    for (int j = 0; j < gr.nd; ++j) {
+        const int x = (gr.dlo + j) / M.DNE - gr.dlo / M.DNE;
         P.push_back({kEvPrepareUpTo, x, 0, 0});
         if (M.naq == 2 || (M.mutate & MONOMOE_SCHEDULE_MUTATE_PREFETCH_ONE_BUFFER)) P.push_back({kEvPrefetch, x, 0, 0});
         const int v = M.IP >= NC ? -1 : (j % NC);
@@ -185,7 +193,6 @@ void build(Model& M) {
     M.act.assign(n_up, 0);
     M.act_slot.assign(M.U, 0);
     M.contrib.assign(n_dn, 0);
-    M.dn_owner.assign(n_dn, 0);
     M.g.resize(M.G);
     const int nchunk = (M.H / 16) * ((M.T + 3) / 4);
     for (int wg = 0; wg < M.G; ++wg) {
@@ -193,10 +200,8 @@ void build(Model& M) {
         gr.wg = wg;
         gr.nu = up_count(wg, M.G, n_up);
         gr.dlo = range_lo(wg, M.G, n_dn);
-        gr.dhi = range_lo(wg + 1, M.G, n_dn);
-        gr.dn_u0 = gr.dhi > gr.dlo ? gr.dlo / M.DNE : 0;
-        gr.nx = gr.dhi > gr.dlo ? (gr.dhi - 1) / M.DNE - gr.dn_u0 + 1 : 0;
-        for (int m = gr.dlo; m < gr.dhi; ++m) M.dn_owner[m] = wg;
+        gr.nd = range_lo(wg + 1, M.G, n_dn) - gr.dlo;
+        gr.nx = gr.nd > 0 ? (gr.dlo + gr.nd - 1) / M.DNE - gr.dlo / M.DNE + 1 : 0;
         gr.f_cnt.assign(M.nslots, 0);
         gr.part.assign((size_t)M.nslots * NC, -1);
         int nbar = 0;
@@ -238,13 +243,6 @@ void build(Model& M) {
     }
 }
 
-enum : int {   // violation kinds (monomoe_schedule_report_t.first_violation)
-    kVioSlotOverwrite = 1,   // a hand-off slot rewritten before the helper consumed it
-    kVioSlotStale = 2,       // the helper consumed a slot that does not hold the expected sums
-    kVioBufferRead = 3,      // a compute wavefront read an activation buffer holding another expert
-    kVioBufferOverwrite = 4, // an activation buffer rewritten while a compute wavefront reads it
-    kVioDuplicate = 5,       // a gate/up or down unit published twice (partition overlap)
-};
 
 // Try to execute wavefront (gr, wv)'s next step; false when it is blocked (or ended).
 bool step(Model& M, Group& gr, int wv) {
@@ -256,14 +254,14 @@ bool step(Model& M, Group& gr, int wv) {
     // by group as they complete, blocking or not), so the buffer must be free at every attempt;
     // an attempt that stops early leaves it partly written
     auto prepare = [&](int x) -> bool {
-        const int b = buf(x);
+        const int b = buf(x), u = gr.dlo / M.DNE + x;
         for (int v = 0; v < NC; ++v)
             if (gr.w[v].reading >= 0 && gr.w[v].reading != x && buf(gr.w[v].reading) == b) M.violate(kVioBufferOverwrite);
-        if (M.act_slot[gr.dn_u0 + x] < M.UPE) {   // an activation group of the expert is not complete
+        if (M.act_slot[u] < M.UPE) {   // an activation group of the expert is not complete
             gr.content[b] = -2;
             return false;
         }
-        gr.content[b] = x;
+        gr.content[b] = u;
         gr.f_aq_seq[b] = x + 1;
         return true;
     };
@@ -305,14 +303,14 @@ bool step(Model& M, Group& gr, int wv) {
         case kEvWaitAq: {
             const int b = buf(s.a);
             if (!(M.mutate & MONOMOE_SCHEDULE_MUTATE_NO_ACT_WAIT) && gr.f_aq_seq[b] < s.a + 1) return false;
-            if (gr.content[b] != s.a) M.violate(kVioBufferRead);
+            if (gr.content[b] != s.c) M.violate(kVioBufferRead);
             W.reading = s.a;
             break;
         }
         case kEvHandoff: {
             const int slot = s.a & smask;
             if (!(M.mutate & MONOMOE_SCHEDULE_MUTATE_NO_SLOT_WAIT) && gr.f_consumed < s.a - smask) return false;
-            if (s.b >= 0 && gr.content[buf(s.b)] != s.b) M.violate(kVioBufferOverwrite);
+            if (s.b >= 0 && gr.content[buf(s.b)] != s.c) M.violate(kVioBufferOverwrite);
             const int prev = gr.part[slot * NC + wv];
             if (prev >= 0 && gr.f_consumed <= prev) M.violate(kVioSlotOverwrite);
             gr.part[slot * NC + wv] = s.a;

@@ -117,8 +117,9 @@ def run(args):
 # sources of each kernel (counters and traces are only valid for this code)
 KERNEL_SOURCES = {
     "single": ("csrc/monomoe_kernel.hip", "csrc/monomoe_kernel_one.hip", "csrc/monomoe_fused.h",
-               "csrc/monomoe_device.h", "csrc/monomoe_internal.h"),
-    "multi": ("csrc/monomoe_kernel_mt.hip", "csrc/monomoe_device.h", "csrc/monomoe_internal.h"),
+               "csrc/monomoe_device.h", "csrc/monomoe_internal.h", "csrc/monomoe_partition.h"),
+    "multi": ("csrc/monomoe_kernel_mt.hip", "csrc/monomoe_device.h", "csrc/monomoe_internal.h",
+              "csrc/monomoe_partition.h"),
 }
 
 
