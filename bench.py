@@ -24,8 +24,10 @@ reported beside the kernel time.
 Printed (one JSON line): value = algorithmic bytes / summed launch time (GB/s) of the headline
 layer over its token counts; per-T latency (mean, p10/p50/p90, graph replay p50), achieved GB/s
 and fraction of the 8 TB/s peak; the same block for every layer under "workloads"; a roofline
-object for the headline kernel; the CPU oracle on a bounded sample of the headline layer, on
-one host core and on all of them.
+object for the headline kernel, which also carries the device's achievable HBM read rate
+measured in the same run (a plain streaming-read kernel over 2 GiB) and the value's fraction of
+it; the CPU oracle on a bounded sample of the headline layer, on one host core and on all of
+them.
 
 Other layers and token counts (up to 64, where the multi-tile kernel runs) are a flag away:
 `--workloads coarse --tokens 16,32,64`; each layer's routing policy (softmax, or sigmoid with a
@@ -284,6 +286,30 @@ class Workload:
             p.close()
 
 
+def read_ceiling(dev, gib=2, reps=10):
+    """Achievable HBM read rate of this device: monomoe_stream_read (each workgroup reads one
+    contiguous chunk, sixteen 16-byte loads in flight per thread) over a fresh `gib` GiB
+    buffer, event-timed; the median of `reps` launches after three warm-ups, in GB/s."""
+    import torch
+    from paper_2609_04244_amd import monomoe as mm
+    n = gib << 30
+    src = torch.ones(n, dtype=torch.uint8, device=dev)
+    sink = torch.zeros(16, dtype=torch.uint8, device=dev)
+    evs = []
+    for r in range(3 + reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        mm.stream_read(src, sink, n)
+        b.record()
+        if r >= 3:
+            evs.append((a, b))
+    torch.cuda.synchronize()
+    ms = sorted(a.elapsed_time(b) for a, b in evs)
+    del src
+    torch.cuda.empty_cache()
+    return n / (ms[len(ms) // 2] * 1e6)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -348,6 +374,8 @@ def main():
                 w.graph_ms[T].append(a.elapsed_time(b) / w.n)
             w.status_ok()
 
+    ceiling = read_ceiling(dev)
+
     blocks = {}
     head = None
     for w in wls:
@@ -381,6 +409,10 @@ def main():
             "algorithmic_bytes_per_launch": blk0["algorithmic_bytes_per_launch"],
             "kernel": blk0["kernel"],
             "launch_us_mean": blk0["launch_us_mean"],
+            "read_ceiling": round(float(ceiling), 1),
+            "frac_of_read_ceiling": round(float(value / ceiling), 4),
+            "read_ceiling_note": "achievable HBM read rate measured in the same run: monomoe_stream_read, "
+                                 "2 GiB, per-workgroup contiguous chunks, median of 10",
         },
         "wall_s_timed": round(wall, 3),
     }
