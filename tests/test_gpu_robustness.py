@@ -42,6 +42,9 @@ CASES = [
     ("many_tiny_expert", 4, None, "general kernel, biased routing, 256 experts"),
     ("wide_fine", 8, [0, 7], "general kernel, input quantised once and exchanged"),
     ("coarse", 32, [0, 31], "multi-tile kernel"),
+    ("small_expert", 64, [0, 63], "multi-tile kernel"),
+    ("many_tiny_expert", 48, [0, 47], "multi-tile kernel"),
+    ("sigmoid_h7168_tp8", 4, [0, 3], "general kernel, sigmoid routing with selection bias"),
 ]
 
 
@@ -51,9 +54,11 @@ def test_perturbed_launches_are_bit_identical(name, T, tokens, path):
     plan = mm.Plan(T, inp["H"], inp["E"], inp["I"], inp["k"], inp["renorm"], perturb=True)
     if inp["bias"] is not None:
         plan.set_router_bias(inp["bias"])
+    if inp.get("policy", "softmax") == "sigmoid_bias":
+        plan.set_routing(mm.ROUTING_SIGMOID_BIAS, inp["sel_bias"], inp["route_scale"])
     info = plan.info()
     log("case %s T=%d (%s): grid %d, multi_tile %d" % (name, T, path, info["grid"], info["multi_tile"]))
-    assert bool(info["multi_tile"]) == (path == "multi-tile kernel")
+    assert bool(info["multi_tile"]) == path.startswith("multi-tile")
     ref = launch(plan, inp, 0)
     plain = [launch(plan, inp, 0)["us"] for _ in range(3)]
     perturbed = []
