@@ -177,11 +177,19 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
     MONOMOE_PERTURB(0, 0);
 
     // ---------------- stage 0: router slice + input quantisation slice ----------------
+    // A large input is quantised once, split over the workgroups, and exchanged (see below);
+    // each workgroup publishes its share first, so that the shares travel while the router
+    // rows are computed.
+    const bool xq_exchange = !ONE && T * (H / 8) > kLocalQuantChunks * kThreads;
+    static_assert(4 * (H / 8) <= kLocalQuantChunks * kThreads, "the input exchange starts above four tokens");
     if (ONE || T == 1) router_rows<H, 1>(p, wg, G, tid, tag, red);
     else if (T == 2) router_rows<H, 2>(p, wg, G, tid, tag, red);
     else if (T <= 4) router_rows<H, 4>(p, wg, G, tid, tag, red);
-    else if (T <= 8) router_rows<H, 8>(p, wg, G, tid, tag, red);
-    else router_rows<H, kTMax>(p, wg, G, tid, tag, red);
+    else {
+        if (xq_exchange) publish_input_groups<H>(p, T, wg, G, tid, tag);   // (T > 4 only)
+        if (T <= 8) router_rows<H, 8>(p, wg, G, tid, tag, red);
+        else router_rows<H, kTMax>(p, wg, G, tid, tag, red);
+    }
     if (tid == 0) stamp(p.stamps, wg, kStRouter);
     // One token (the ONE specialisation, launched for T = 1 without the timeout test hook):
     // its selected experts are the active experts, one slot per top-k position, so the work
@@ -231,12 +239,10 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
         // Input quantisation.  A small input (at most kLocalQuantChunks chunks per thread) is
         // quantised by every workgroup into its own LDS while the other router rows complete
         // (no exchange, and the work hides behind the logit wait).  A larger one is quantised
-        // once, split over the workgroups, and fetched back (publish_input_groups /
-        // fetch_input): one round trip instead of G-fold replicated arithmetic.
-        const bool xq_exchange = T * (H / 8) > kLocalQuantChunks * kThreads;
+        // once, split over the workgroups (published before the router rows, above), and
+        // fetched back: one round trip instead of G-fold replicated arithmetic.
         bool xq_ok = true;
         if (xq_exchange) {
-            publish_input_groups<H>(p, T, wg, G, tid, tag);
             xq_ok = fetch_input<H>(p, T, xq_s, xs_s, tid, tag, status, limit);
         } else {
             quantise_input<H>(p.x, T, xq_s, xs_s, tid, wg == 0 ? p.d_xq : nullptr, p.d_xs);

@@ -209,6 +209,7 @@ void build(Model& M) {
             std::vector<Step>& P = gr.w[wv].prog;
             int b = 0;
             P.push_back({kEvBarrier, b++, 0, 0});   // flags initialised
+            if (M.exchange) P.push_back({kEvPublishGroups, 0, 0, 0});   // the input share, first
             // stage 0: router rows e = wg, wg + G, ... (two workgroup barriers each; the
             // first wavefront's lanes store the row)
             for (int e = wg; e < M.E; e += M.G) {
@@ -224,10 +225,7 @@ void build(Model& M) {
                     P.push_back({kEvQuantDone, 0, 0, 0});
                 }
             } else {
-                if (M.exchange) {
-                    P.push_back({kEvPublishGroups, 0, 0, 0});
-                    P.push_back({kEvWaitGroups, 0, 0, 0});
-                }
+                if (M.exchange) P.push_back({kEvWaitGroups, 0, 0, 0});
                 if (2 * wv < M.T) P.push_back({kEvWaitRows, 0, 0, 0});   // this wavefront's tokens
                 for (int i = 0; i < 3; ++i) P.push_back({kEvBarrier, b++, 0, 0});   // top-k, masks, metadata
             }
