@@ -243,6 +243,8 @@ typedef struct {
     int32_t multi_tile;      /* 1 when the multi-tile kernel runs, else 0             */
     int32_t group_tokens;    /* multi-tile: R, the most tokens of one expert segment  */
     int32_t down_slices;     /* multi-tile: K slices of the down projection           */
+    int32_t up_block;        /* single-tile: gate/up units per deal of the schedule   */
+    int32_t down_grid;       /* single-tile: workgroups with down units               */
 } monomoe_plan_info_t;
 
 int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info);
@@ -260,11 +262,20 @@ int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info);
  *   general_only: single-tile only; 0 (default) runs passes of one token on the kernel's
  *         one-token specialisation (the selected experts are the active ones, so each
  *         workgroup starts streaming as soon as the experts it needs are ranked), 1 runs
- *         them on the general kernel.
- * The task size and the per-expert workgroup groups follow from the weight-major partition
- * and are not separate parameters.  Schedules that differ only in grid, ring or
- * general_only compute bit-identical outputs; the kernel choice and R change the order of
- * fp32 summation only.
+ *         them on the general kernel;
+ *   up_block: single-tile only; gate/up units (8 gate + 8 up rows of one expert) dealt to a
+ *         workgroup at a time, round-robin over the grid: 1 (0 = the default), 2, 4 or 8.
+ *         An expert's I/8 units are spread over about I/(8 up_block) workgroups: the
+ *         workgroups per expert of the gate/up phase (the paper's G_up);
+ *   down_grid: single-tile only; the workgroups that run the down projection (the first
+ *         down_grid of the grid take contiguous ranges of its 16-row units; 0 = the whole
+ *         grid), so that an expert's H/16 down units are spread over about down_grid / U
+ *         workgroups for U active experts (the paper's G_down).  At most grid.
+ * The task depth (256 deep per ring slot) and the single ring running through both phases
+ * are fixed by the design (a ring slot is 16 registers; the first down tasks are in flight
+ * while the last gate/up tasks compute).  Schedules that differ only in grid, ring,
+ * general_only, up_block or down_grid compute bit-identical outputs; the kernel choice and
+ * R change the order of fp32 summation only.
  * A new grid resets the plan's workspace (blocking; no launch of the plan may be pending).
  * Returns MONOMOE_ERR_INVALID (plan unchanged) for an out-of-range field, and
  * MONOMOE_ERR_UNSUPPORTED when the requested kernel cannot hold the shape's tiles. */
@@ -275,6 +286,8 @@ typedef struct {
     int32_t kernel;
     int32_t group_tokens;
     int32_t general_only;
+    int32_t up_block;
+    int32_t down_grid;
 } monomoe_schedule_t;
 int monomoe_plan_set_schedule(monomoe_plan_t plan, const monomoe_schedule_t* sched);
 
@@ -322,6 +335,8 @@ int monomoe_layout(const monomoe_shape_t* shape, int topk, int kernel, int lds_t
  *                    per token (the order within a token is its top-k order)
  *   one_token        1: the one-token specialisation (T must be 1); 0: the general kernel
  *   grid, ring       persistent workgroups (<= 1024) and weight-ring depth (2 or 4)
+ *   up_block, down_grid  the schedule's work partition (monomoe_plan_set_schedule: 0, 1, 2,
+ *                    4 or 8 gate/up units per deal; 0 or 1 .. grid workgroups with down units)
  *   handoff_slots, act_buffers   the LDS layout (monomoe_layout: a power of two <= 32; 1 or 2)
  *   mutate           0 for the kernel's protocol; MONOMOE_SCHEDULE_MUTATE_* bits remove a
  *                    wait or move a step, so that a test can show the check catches the
@@ -346,7 +361,8 @@ typedef struct {
 } monomoe_schedule_report_t;
 
 int monomoe_schedule_check(const monomoe_shape_t* shape, int topk, const int32_t* topk_ids, int one_token,
-                           int grid, int ring, int handoff_slots, int act_buffers, int resident, uint32_t seed,
+                           int grid, int ring, int up_block, int down_grid, int handoff_slots, int act_buffers,
+                           int resident, uint32_t seed,
                            uint32_t mutate, monomoe_schedule_report_t* out);
 
 /* 1 if (H, I) is one of the compiled shapes, else 0. */

@@ -46,6 +46,8 @@ struct monomoe_plan_s {
     int mt;       // multi-tile kernel
     int mt_rows, mt_pool, mt_tiles;
     int general_only;           // schedule: no one-token specialisation
+    int up_lb;                  // schedule: gate/up units per deal 2^up_lb (single-tile kernel)
+    int down_grid;              // schedule: workgroups with down units (0: the whole grid)
     KernelConfig cfg;           // the configuration above, as chosen for T
     KernelConfig small;         // single-tile configuration for forwards of at most small_T
     int small_T;                //   tokens when cfg is the multi-tile kernel (0: none)
@@ -359,8 +361,10 @@ int launch(monomoe_plan_t plan, int T, const void* x, const void* router_w, cons
     p.E = s.E;
     p.k = plan->topk;
     p.renorm = plan->renorm;
-    p.naq = cf.naq;
-    p.nslots = cf.nslots;
+    p.naq = (int16_t)cf.naq;
+    p.nslots = (int16_t)cf.nslots;
+    p.up_lb = (uint8_t)plan->up_lb;
+    p.dn_grid = (uint16_t)(plan->down_grid ? plan->down_grid : plan->grid);
     p.mt_rows = (uint8_t)cf.rows;
     p.mt_tiles = (uint8_t)cf.tiles;
     p.mt_pool = (uint16_t)cf.pool;
@@ -614,6 +618,10 @@ int monomoe_plan_set_schedule(monomoe_plan_t plan, const monomoe_schedule_t* sch
     if (sched->group_tokens < 0 || sched->group_tokens > kTLimit) return MONOMOE_ERR_INVALID;
     if (sched->ring != 0 && sched->ring != kRings[0] && sched->ring != kRings[1]) return MONOMOE_ERR_INVALID;
     if (sched->general_only != 0 && sched->general_only != 1) return MONOMOE_ERR_INVALID;
+    int up_lb = 0;
+    while (up_lb < kUpBlockLogMax && (1 << up_lb) < sched->up_block) ++up_lb;
+    if (sched->up_block < 0 || (sched->up_block > 0 && (1 << up_lb) != sched->up_block)) return MONOMOE_ERR_INVALID;
+    if (sched->down_grid < 0) return MONOMOE_ERR_INVALID;
     int dev = -1;
     if (hipGetDevice(&dev) != hipSuccess || dev != plan->device) return MONOMOE_ERR_INVALID;
     KernelConfig cfg{}, small{};
@@ -622,6 +630,7 @@ int monomoe_plan_set_schedule(monomoe_plan_t plan, const monomoe_schedule_t* sch
     if (cr != MONOMOE_OK) return cr;
     const int grid = sched->grid == 0 ? plan->num_cus : sched->grid;
     if (grid < 1 || grid > plan->num_cus * cfg.occupancy || grid > kGridMax) return MONOMOE_ERR_INVALID;
+    if (sched->down_grid > grid) return MONOMOE_ERR_INVALID;
     if (small_T > 0 && grid > plan->num_cus * small.occupancy) small_T = 0;
     // the launch epochs are per workgroup: a new grid starts from a clean workspace
     if (grid != plan->grid) {
@@ -631,6 +640,8 @@ int monomoe_plan_set_schedule(monomoe_plan_t plan, const monomoe_schedule_t* sch
     }
     plan->grid = grid;
     plan->general_only = sched->general_only;
+    plan->up_lb = up_lb;
+    plan->down_grid = sched->down_grid == grid ? 0 : sched->down_grid;
     apply_config(plan, cfg, small, small_T);
     return MONOMOE_OK;
 }
@@ -725,6 +736,8 @@ int monomoe_plan_info(monomoe_plan_t plan, monomoe_plan_info_t* info) {
     info->multi_tile = c.mt;
     info->group_tokens = c.mt ? c.rows : 0;
     info->down_slices = c.mt ? (plan->shape.I / 128) / mt_slice_blocks(plan->shape.I / 128) : 1;
+    info->up_block = 1 << plan->up_lb;
+    info->down_grid = plan->down_grid ? plan->down_grid : plan->grid;
     return MONOMOE_OK;
 }
 

@@ -323,19 +323,22 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
     }
 
     // ---------------- work partition (identical in every wavefront) ----------------
-    // Gate/up units are dealt round-robin over the workgroups: the j-th unit of workgroup
-    // wg is unit wg + G*j.  Each expert's units are spread over many workgroups and every
+    // Gate/up units are dealt round-robin over the workgroups (by default single units: the
+    // j-th unit of workgroup wg is unit wg + G*j; the schedule may deal blocks of 2^up_lb
+    // consecutive units instead).  Each expert's units are spread over many workgroups and every
     // workgroup works through the experts in slot order, so all workgroups stream the same
     // few experts at a time and the act rows complete expert by expert through the phase
     // (and with one token every workgroup starts on one of the first selections).  Down
     // units are split into contiguous ranges (one or two experts per workgroup, so each
-    // workgroup requantises one or two act rows).
+    // workgroup requantises one or two act rows) over the first Gd workgroups (by default
+    // the whole grid).
     const int n_up = U * UPE, n_dn = U * DNE;
     static_assert((uint64_t)kUMax * (H / 16) * kGridMax < (1ull << 32) &&
-                      (uint64_t)kUMax * (I / 8) + kGridMax < (1ull << 31), "partition arithmetic");
-    const int nu = up_count(wg, G, n_up);                     // gate/up units of this workgroup
-    const int dlo = range_lo(wg, G, n_dn);
-    const int dhi = range_lo(wg + 1, G, n_dn);
+                      (uint64_t)kUMax * (I / 8) + ((uint64_t)kGridMax << kUpBlockLogMax) < (1ull << 31), "partition arithmetic");
+    const int ulb = p.up_lb, Gd = p.dn_grid;
+    const int nu = up_count(wg, G, n_up, ulb);                // gate/up units of this workgroup
+    const int dlo = down_lo(wg, Gd, n_dn);
+    const int dhi = down_lo(wg + 1, Gd, n_dn);
     const int nd = dhi - dlo;                                 // down units of this workgroup
     const int dn_u0 = nd > 0 ? dlo / DNE : 0;                 // first expert slot of the down range
 
@@ -422,7 +425,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
         auto lbase = [&]() MONOMOE_CURSOR_INLINE {   // per-lane addresses of task lkp of unit lm
             const int kb = 2 * lkp;
             if (lph == 0) {
-                const int mu = up_unit(wg, G, lm);   // the unit
+                const int mu = up_unit(wg, G, lm, ulb);   // the unit
                 const int u = mu / UPE, i0 = (mu - u * UPE) * 8;
                 if constexpr (ONE) ranked(u);
                 const int e = ONE ? min(max(uni(sel_ids[u]), 0), E - 1) : uni(act_e[u]);
@@ -604,7 +607,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
 
         // --- gate/up epilogues: SiLU(gate)*up, stored as tagged words ---
         for (int j = 0; j < nu; ++j) {
-            const int m = up_unit(wg, G, j), slot = j & smask;
+            const int m = up_unit(wg, G, j, ulb), slot = j & smask;
             if (!wait_lds(&f_cnt[slot], NCU, &f_abort, limit)) { fine = false; break; }
             const int u = m / UPE, i0 = (m - u * UPE) * 8;
             const uint32_t tmask = act_m[u];

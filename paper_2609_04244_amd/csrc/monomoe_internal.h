@@ -19,6 +19,7 @@ constexpr int kSlotsMin = 4;                  // partial-sum hand-off slots per 
 constexpr int kSlotsMax = 32;                 //   a power of two in [min, max], as LDS allows
 
 constexpr int kGridMax = 1024;                // persistent workgroups at most
+constexpr int kUpBlockLogMax = 3;             // gate/up units per deal at most: 2^3 (schedule)
 
 // Multi-tile kernel (more tokens than one 16-wide N tile): tokens are compacted per
 // active expert and processed in segments of at most R tokens, each segment on up to
@@ -95,8 +96,12 @@ struct KParams {
     int32_t T, E, k, renorm;
     int32_t policy;           // MONOMOE_ROUTING_SOFTMAX / MONOMOE_ROUTING_SIGMOID_BIAS
     float route_scale;        // routed scaling factor (sigmoid routing)
-    int32_t naq;              // requantised-act LDS buffers (2 = double buffered, 1)
-    int32_t nslots;           // partial-sum hand-off slots (power of two)
+    int16_t naq;              // requantised-act LDS buffers (2 = double buffered, 1)
+    int16_t nslots;           // partial-sum hand-off slots (power of two)
+    // single-tile kernel's work partition (schedule; monomoe_partition.h)
+    uint8_t up_lb;            // gate/up units per deal: 2^up_lb
+    uint8_t pad0;
+    uint16_t dn_grid;         // workgroups with down units (the first dn_grid of the grid)
     // multi-tile kernel only (packed into the struct's tail padding)
     uint8_t mt_rows;          // R: tokens per segment at most (<= kTLimit)
     uint8_t mt_tiles;         // N tiles per hand-off slot entry: ceil(R / 16)

@@ -86,6 +86,7 @@ struct Group {
 struct Model {
     // shape and schedule
     int T, H, E, I, K, G, nslots, naq, one, ring;
+    int ulb, Gd;                  // work partition: gate/up deal block 2^ulb, down workgroups
     int U, UPE, DNE, HP, IP, NCU, NCD;
     uint32_t mutate;
     bool exchange;
@@ -134,7 +135,7 @@ void build_compute(Model& M, Group& gr, int wv) {
         for (int i = 0; i < c; ++i) tasks.push_back({1, m});
     }
     auto slot_of = [&](const Task& t) {   // expert slot of a task's unit
-        return t.ph == 0 ? up_unit(gr.wg, M.G, t.m) / M.UPE : (gr.dlo + t.m) / M.DNE;
+        return t.ph == 0 ? up_unit(gr.wg, M.G, t.m, M.ulb) / M.UPE : (gr.dlo + t.m) / M.DNE;
     };
     auto new_unit = [&](size_t i) { return i == 0 || tasks[i].ph != tasks[i - 1].ph || tasks[i].m != tasks[i - 1].m; };
     auto lbase = [&](size_t i) {   // load cursor entering task i
@@ -176,7 +177,7 @@ void build_helper(Model& M, Group& gr) {
     for (int j = 0; j < gr.nu; ++j) {
         const int v = M.HP >= NC ? -1 : (j % NC);
         P.push_back({kEvConsume, j, M.NCU, v});
-        P.push_back({kEvPublishAct, up_unit(gr.wg, M.G, j), 0, 0});
+        P.push_back({kEvPublishAct, up_unit(gr.wg, M.G, j, M.ulb), 0, 0});
     }
     for (int j = 0; j < gr.nd; ++j) {
         const int x = (gr.dlo + j) / M.DNE - gr.dlo / M.DNE;
@@ -198,9 +199,9 @@ void build(Model& M) {
     for (int wg = 0; wg < M.G; ++wg) {
         Group& gr = M.g[wg];
         gr.wg = wg;
-        gr.nu = up_count(wg, M.G, n_up);
-        gr.dlo = range_lo(wg, M.G, n_dn);
-        gr.nd = range_lo(wg + 1, M.G, n_dn) - gr.dlo;
+        gr.nu = up_count(wg, M.G, n_up, M.ulb);
+        gr.dlo = down_lo(wg, M.Gd, n_dn);
+        gr.nd = down_lo(wg + 1, M.Gd, n_dn) - gr.dlo;
         gr.nx = gr.nd > 0 ? (gr.dlo + gr.nd - 1) / M.DNE - gr.dlo / M.DNE + 1 : 0;
         gr.f_cnt.assign(M.nslots, 0);
         gr.part.assign((size_t)M.nslots * NC, -1);
@@ -374,14 +375,16 @@ uint32_t next_rand(uint64_t& st) {   // xorshift64*
 using namespace monomoe;
 
 extern "C" int monomoe_schedule_check(const monomoe_shape_t* shape, int topk, const int32_t* topk_ids,
-                                      int one_token, int grid, int ring, int handoff_slots, int act_buffers,
-                                      int resident, uint32_t seed, uint32_t mutate,
+                                      int one_token, int grid, int ring, int up_block, int down_grid,
+                                      int handoff_slots, int act_buffers, int resident, uint32_t seed,
+                                      uint32_t mutate,
                                       monomoe_schedule_report_t* out) {
     if (!shape || !topk_ids || !out) return MONOMOE_ERR_INVALID;
     const int T = shape->T, H = shape->H, E = shape->E, I = shape->I;
     if (T < 1 || H < 256 || I < 256 || H % 256 || I % 256 || E < 1 || E > kEMax || topk < 1 || topk > kKMax ||
         topk > E || grid < 1 || grid > kGridMax || resident < 1 || (one_token != 0 && one_token != 1) ||
-        (ring != kRings[0] && ring != kRings[1]) ||
+        (ring != kRings[0] && ring != kRings[1]) || down_grid < 0 || down_grid > grid ||
+        (up_block != 0 && up_block != 1 && up_block != 2 && up_block != 4 && up_block != 8) ||
         handoff_slots < 1 || (handoff_slots & (handoff_slots - 1)) || handoff_slots > kSlotsMax ||
         (act_buffers != 1 && act_buffers != 2) || (mutate & ~7u))
         return MONOMOE_ERR_INVALID;
@@ -389,6 +392,8 @@ extern "C" int monomoe_schedule_check(const monomoe_shape_t* shape, int topk, co
     Model M;
     M.T = T, M.H = H, M.E = E, M.I = I, M.K = topk, M.G = grid, M.nslots = handoff_slots, M.naq = act_buffers;
     M.one = one_token, M.ring = ring, M.mutate = mutate;
+    M.ulb = up_block >= 8 ? 3 : up_block >= 4 ? 2 : up_block >= 2 ? 1 : 0;
+    M.Gd = down_grid == 0 ? grid : down_grid;
     M.UPE = I / 8, M.DNE = H / 16, M.HP = H / 256, M.IP = I / 256;
     M.NCU = M.HP < NC ? 1 : NC, M.NCD = M.IP < NC ? 1 : NC;
     M.exchange = !one_token && T * (H / 8) > kLocalQuantChunks * kThreads;

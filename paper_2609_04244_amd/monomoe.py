@@ -61,12 +61,14 @@ class PlanInfo(ctypes.Structure):
     _fields_ = [("grid", ctypes.c_int32), ("block", ctypes.c_int32), ("lds_bytes", ctypes.c_int32),
                 ("occupancy", ctypes.c_int32), ("num_cus", ctypes.c_int32), ("workspace_bytes", ctypes.c_int64),
                 ("scratch_bytes", ctypes.c_int32), ("ring", ctypes.c_int32), ("tokens_per_pass", ctypes.c_int32),
-                ("multi_tile", ctypes.c_int32), ("group_tokens", ctypes.c_int32), ("down_slices", ctypes.c_int32)]
+                ("multi_tile", ctypes.c_int32), ("group_tokens", ctypes.c_int32), ("down_slices", ctypes.c_int32),
+                ("up_block", ctypes.c_int32), ("down_grid", ctypes.c_int32)]
 
 
 class Schedule(ctypes.Structure):
     _fields_ = [("grid", ctypes.c_int32), ("ring", ctypes.c_int32), ("kernel", ctypes.c_int32),
-                ("group_tokens", ctypes.c_int32), ("general_only", ctypes.c_int32)]
+                ("group_tokens", ctypes.c_int32), ("general_only", ctypes.c_int32), ("up_block", ctypes.c_int32),
+                ("down_grid", ctypes.c_int32)]
 
 
 class ScheduleReport(ctypes.Structure):
@@ -117,7 +119,7 @@ def _load(path):
         L.monomoe_plan_set_schedule.restype = ctypes.c_int
         L.monomoe_layout.argtypes = [ctypes.POINTER(Shape)] + [ctypes.c_int] * 7 + [ctypes.POINTER(Layout)]
         L.monomoe_layout.restype = ctypes.c_int
-        L.monomoe_schedule_check.argtypes = [ctypes.POINTER(Shape), ctypes.c_int, vp] + [ctypes.c_int] * 6 + \
+        L.monomoe_schedule_check.argtypes = [ctypes.POINTER(Shape), ctypes.c_int, vp] + [ctypes.c_int] * 8 + \
             [ctypes.c_uint32, ctypes.c_uint32, ctypes.POINTER(ScheduleReport)]
         L.monomoe_schedule_check.restype = ctypes.c_int
         L.monomoe_forward.argtypes = [vp] * 9
@@ -162,7 +164,7 @@ def layout(T, H, E, I, topk, kernel, lds_total, lds_static, occupancy, grid=0, n
 
 
 def schedule_check(ids, H, E, I, one_token, grid, ring, handoff_slots, act_buffers, resident=None, seed=0,
-                   mutate=0):
+                   mutate=0, up_block=0, down_grid=0):
     """monomoe_schedule_check (host model of the single-tile kernel's hand-offs, no device) for
     the selection `ids` (int array [T, topk]): (status code, report dict or None)."""
     import numpy as np
@@ -170,7 +172,8 @@ def schedule_check(ids, H, E, I, one_token, grid, ring, handoff_slots, act_buffe
     T, k = ids.shape
     out = ScheduleReport()
     rc = lib().monomoe_schedule_check(ctypes.byref(Shape(T, H, E, I)), k, ids.ctypes.data_as(ctypes.c_void_p),
-                                      int(one_token), int(grid), int(ring), int(handoff_slots), int(act_buffers),
+                                      int(one_token), int(grid), int(ring), int(up_block), int(down_grid),
+                                      int(handoff_slots), int(act_buffers),
                                       int(grid if resident is None else resident), int(seed), int(mutate),
                                       ctypes.byref(out))
     return rc, ({f: getattr(out, f) for f, _ in ScheduleReport._fields_} if rc == MONOMOE_OK else None)
@@ -316,12 +319,16 @@ class Plan:
             raise MonoMoEError(rc, "monomoe_plan_set_routing")
         self._sel_bias = sel_bias  # keep the tensor alive while the plan refers to it
 
-    def set_schedule(self, grid=0, ring=0, kernel=KERNEL_AUTO, group_tokens=0, general_only=0):
+    def set_schedule(self, grid=0, ring=0, kernel=KERNEL_AUTO, group_tokens=0, general_only=0, up_block=0,
+                     down_grid=0):
         """Persistent grid (0 = one workgroup per CU), weight-ring depth (0 = default), kernel
-        (KERNEL_AUTO / KERNEL_SINGLE / KERNEL_MULTI), the multi-tile segment cap (0 = none), and
+        (KERNEL_AUTO / KERNEL_SINGLE / KERNEL_MULTI), the multi-tile segment cap (0 = none),
         general_only (1: passes of one token on the general single-tile kernel, not its
-        one-token specialisation)."""
-        sch = Schedule(int(grid), int(ring), int(kernel), int(group_tokens), int(general_only))
+        one-token specialisation), and the single-tile kernel's work partition: gate/up units
+        per deal (up_block: 0 = 1, 2, 4, 8) and the workgroups with down units (down_grid:
+        0 = the whole grid)."""
+        sch = Schedule(int(grid), int(ring), int(kernel), int(group_tokens), int(general_only), int(up_block),
+                       int(down_grid))
         rc = self._L.monomoe_plan_set_schedule(self._h, ctypes.byref(sch))
         if rc != MONOMOE_OK:
             raise MonoMoEError(rc, "monomoe_plan_set_schedule")

@@ -2,10 +2,13 @@
 precompiled for a set of schedules; candidates that fail numerical validation are
 rejected and the rest ranked by latency over the target token-count range).
 
-A schedule here is (kernel, grid, ring, one-token specialisation, segment cap): the
-single-tile or multi-tile kernel, the persistent workgroup count, the weight-ring depth,
-whether passes of one token run on the single-tile kernel's one-token specialisation, and
-the multi-tile kernel's cap on tokens per expert segment (see monomoe_plan_set_schedule).
+A schedule here is (kernel, grid, ring, one-token specialisation, segment cap, gate/up deal
+block, down workgroups): the single-tile or multi-tile kernel, the persistent workgroup
+count, the weight-ring depth, whether passes of one token run on the single-tile kernel's
+one-token specialisation, the multi-tile kernel's cap on tokens per expert segment, and the
+single-tile kernel's work partition -- gate/up units dealt to a workgroup at a time (an
+expert's units then spread over about I/(8 block) workgroups: the paper's G_up) and the
+workgroups that run the down projection (the paper's G_down) (see monomoe_plan_set_schedule).
 For one workload and a list of token counts:
 
   1. enumerate the candidates (combinations the plan rejects are dropped: the multi-tile
@@ -18,8 +21,8 @@ For one workload and a list of token counts:
      is what the parity tests check against the fp64 oracle; the package itself does not use
      the oracle, and tests/test_gpu_tuned_schedules.py runs every tuned schedule against it),
      with the device status OK: a candidate that runs the same kernel must be bit-identical
-     (grid, ring and the one-token specialisation change when and where the work runs, never
-     the arithmetic); one that runs the other kernel or caps the segments sums in another
+     (grid, ring, the one-token specialisation and the work partition change when and where
+     the work runs, never the arithmetic); one that runs the other kernel or caps the segments sums in another
      order and must be within the operator's output bound (max |diff| <= 2e-2 rms, mean
      relative difference <= 5e-3);
   3. rank the survivors by the sum over the token counts of the per-launch time of HIP graph
@@ -32,7 +35,7 @@ this file: {workload: {T: schedule}}), which `apply_tuned` reads.
 
 Example:
   python3 -m paper_2609_04244_amd.tune --workload small_expert --T 1,2,4,8 \\
-      --grids 0,192 --rings 2,4 --kernels single,multi --table \\
+      --grids 0,192 --rings 2,4 --up-blocks 1,2,4 --down-grids 0,192 --kernels single,multi --table \\
       --out profiles/schedule_tuning_small_expert.md
 """
 import argparse
@@ -67,7 +70,7 @@ def tuned_schedule(workload, T, path=TABLE):
     """The tuned schedule of `workload` at T tokens (a dict of set_schedule's keyword
     arguments), or None when the table has none."""
     e = load_table(path).get(workload, {}).get(str(T))
-    return None if e is None else {k: e[k] for k in SCHEDULE_KEYS}
+    return None if e is None else {k: e.get(k, 0) for k in SCHEDULE_KEYS}
 
 
 def apply_tuned(plan, workload, T, path=TABLE):
@@ -79,12 +82,12 @@ def apply_tuned(plan, workload, T, path=TABLE):
     return True
 
 
-SCHEDULE_KEYS = ("kernel", "grid", "ring", "general_only", "group_tokens")
+SCHEDULE_KEYS = ("kernel", "grid", "ring", "general_only", "group_tokens", "up_block", "down_grid")
 TIE = 0.01   # a schedule replaces the default at T only when faster by more than this fraction
 KERNEL_NAMES = {mm.KERNEL_SINGLE: "single", mm.KERNEL_MULTI: "multi"}
 
 
-def model_verdict(plan, cfg, T, general_only, seed=0):
+def model_verdict(plan, cfg, T, general_only, seed=0, up_block=0, down_grid=0):
     """The host model check of the plan's single-tile schedule at T tokens: None when every
     pass size runs to completion without a safety violation (a seeded routing each), else the
     reason."""
@@ -100,7 +103,8 @@ def model_verdict(plan, cfg, T, general_only, seed=0):
         ids = np.stack([rng.choice(cfg["E"], size=cfg["k"], replace=False) for _ in range(Tp)])
         one = int(Tp == 1 and not general_only)
         rc, r = mm.schedule_check(ids, cfg["H"], cfg["E"], cfg["I"], one, info["grid"], info["ring"],
-                                  lay["handoff_slots"], lay["act_buffers"], seed=seed + 1)
+                                  lay["handoff_slots"], lay["act_buffers"], seed=seed + 1, up_block=up_block,
+                                  down_grid=down_grid)
         if rc != mm.MONOMOE_OK:
             return "model check: %s" % mm.status_string(rc)
         if not r["complete"] or r["violations"]:
@@ -114,6 +118,10 @@ def label(c):
         s += " general"
     if c[0] == mm.KERNEL_MULTI and c[4]:
         s += " R<=%d" % c[4]
+    if c[0] == mm.KERNEL_SINGLE and c[5] > 1:
+        s += " up%d" % c[5]
+    if c[0] == mm.KERNEL_SINGLE and c[6]:
+        s += " dn%d" % c[6]
     return s
 
 
@@ -125,6 +133,9 @@ def main(argv=None):
     ap.add_argument("--rings", default="2,4")
     ap.add_argument("--kernels", default="single", help="single, multi or both (comma-separated)")
     ap.add_argument("--group-tokens", default="0", help="multi-tile segment caps (0 = none), comma-separated")
+    ap.add_argument("--up-blocks", default="1", help="single-tile gate/up units per deal, comma-separated")
+    ap.add_argument("--down-grids", default="0",
+                    help="single-tile workgroups with down units (0 = the whole grid), comma-separated")
     ap.add_argument("--layers", type=int, default=8)
     ap.add_argument("--replays", type=int, default=6, help="timed graph replays (of --layers launches each)")
     ap.add_argument("--reps", type=int, default=2)
@@ -150,24 +161,29 @@ def main(argv=None):
             plan.set_routing(mm.ROUTING_SIGMOID_BIAS, L["sel_bias"], L["route_scale"])
 
     def schedule(plan, c):
-        plan.set_schedule(kernel=c[0], grid=c[1], ring=c[2], general_only=c[3], group_tokens=c[4])
+        plan.set_schedule(kernel=c[0], grid=c[1], ring=c[2], general_only=c[3], group_tokens=c[4], up_block=c[5],
+                          down_grid=c[6])
 
     kmode = {"single": mm.KERNEL_SINGLE, "multi": mm.KERNEL_MULTI}
     probe = make_plan(Ts[0], layers[0])
     info = probe.info()
     probe.close()
-    # candidate: (kernel, grid, ring, general_only, group_tokens)
+    # candidate: (kernel, grid, ring, general_only, group_tokens, up_block, down_grid); down_grid 0 is
+    # the whole grid
     cands = []
     for kn in args.kernels.split(","):
         for g in (int(x) for x in args.grids.split(",")):
             g = g if g else info["num_cus"]
             if kn == "multi":   # ring depth 2 only; segment caps
                 for R in (int(x) for x in args.group_tokens.split(",")):
-                    cands.append((mm.KERNEL_MULTI, g, 2, 0, R))
+                    cands.append((mm.KERNEL_MULTI, g, 2, 0, R, 1, 0))
             else:
                 for r in (int(x) for x in args.rings.split(",")):
                     for gen in ((0, 1) if 1 in Ts else (0,)):   # the specialisation matters at T = 1 only
-                        cands.append((mm.KERNEL_SINGLE, g, r, gen, 0))
+                        for ub in (int(x) for x in args.up_blocks.split(",")):
+                            for dg in (int(x) for x in args.down_grids.split(",")):
+                                if dg < g:   # (down_grid = grid is the default, 0)
+                                    cands.append((mm.KERNEL_SINGLE, g, r, gen, 0, max(ub, 1), dg))
 
     # 1-2. enumeration and validation gate
     rejected, defaults, one_pass = {}, {}, {}
@@ -180,7 +196,7 @@ def main(argv=None):
         plan = make_plan(T, layers[0])
         dinfo = plan.info()
         dk = mm.KERNEL_MULTI if dinfo["multi_tile"] else mm.KERNEL_SINGLE
-        defaults[T] = (dk, dinfo["grid"], dinfo["ring"], 0, 0)
+        defaults[T] = (dk, dinfo["grid"], dinfo["ring"], 0, 0, 1, 0)
         out = torch.empty((T, cfg["H"]), dtype=torch.bfloat16, device=dev)
         ref = run(plan, layers[0], T, out).clone()
         reff = ref.float()
@@ -194,7 +210,7 @@ def main(argv=None):
                 rejected[c] = "not accepted: %s" % e
                 continue
             if c[0] == mm.KERNEL_SINGLE:
-                why = model_verdict(plan, cfg, T, c[3], seed=T)
+                why = model_verdict(plan, cfg, T, c[3], seed=T, up_block=c[5], down_grid=c[6])
                 if why is not None:
                     rejected[c] = why
                     continue
@@ -269,7 +285,7 @@ def main(argv=None):
     for c in valid:   # schedules identical at T (see above) share its figures
         for T in Ts:
             if c[3] and not one_pass[T]:
-                twin = (c[0], c[1], c[2], 0, c[4])
+                twin = (c[0], c[1], c[2], 0, c[4], c[5], c[6])
                 best_us[(c, T)], best_dsp[(c, T)] = best_us[(twin, T)], best_dsp[(twin, T)]
     ranked = sorted(valid, key=lambda c: sum(best_us[(c, T)] for T in Ts))
 
@@ -292,7 +308,8 @@ def main(argv=None):
               "time of HIP graph replays holding one forward of each of %d rotated layers (median of %d replays), "
               "best of %d repetitions; in brackets the mean dispatch-stamped launch time of the same launches. "
               "Candidates: kernel/grid/ring, 'general' = passes of one token on the general single-tile kernel "
-              "instead of its one-token specialisation, 'R<=n' = multi-tile segment cap." %
+              "instead of its one-token specialisation, 'R<=n' = multi-tile segment cap, 'upB' = gate/up units "
+              "dealt B at a time, 'dnG' = down projection on the first G workgroups." %
               (cfg["H"], cfg["E"], cfg["I"], cfg["k"], info["num_cus"],
                ", ".join("T=%d %s" % (T, label(defaults[T])) for T in Ts), n, args.replays, args.reps), "",
               "| rank | schedule | " + " | ".join("T=%d us" % T for T in Ts) + " | sum us |",
@@ -320,7 +337,7 @@ def main(argv=None):
         ent = tab.setdefault(args.workload, {})
         for T, c in best_T.items():
             grid = 0 if c[1] == info["num_cus"] else c[1]   # 0: one workgroup per CU, on any device
-            ent[str(T)] = dict(zip(SCHEDULE_KEYS, (c[0], grid, c[2], c[3], c[4])), us=round(best_us[(c, T)], 2),
+            ent[str(T)] = dict(zip(SCHEDULE_KEYS, (c[0], grid, c[2], c[3], c[4], c[5], c[6])), us=round(best_us[(c, T)], 2),
                                default_us=round(best_us[(defaults[T], T)], 2) if (defaults[T], T) in best_us else None)
         with open(TABLE, "w") as fh:
             json.dump(tab, fh, indent=1, sort_keys=True)
