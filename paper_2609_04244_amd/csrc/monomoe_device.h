@@ -235,6 +235,17 @@ __device__ __forceinline__ v4f block_mma(const v4i& a0, const v4i& a1, const v4i
     return c;
 }
 
+// block_mma with the A operand already decoded (a[i]: the fp16 values of sub-block i), for a
+// weight block shared by several N tiles: the same products in the same order.
+__device__ __forceinline__ v4f block_mma_a16(const v8h* a, const v4i& b0, const v4i& b1) {
+    v4f c = {0.f, 0.f, 0.f, 0.f};
+    c = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[0], e4m3x8_to_f16(b0[0], b0[1]), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[1], e4m3x8_to_f16(b0[2], b0[3]), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[2], e4m3x8_to_f16(b1[0], b1[1]), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[3], e4m3x8_to_f16(b1[2], b1[3]), c, 0, 0, 0);
+    return c;
+}
+
 // The same 128-deep block contracted by one e4m3 x e4m3 MFMA (16x16x128, both operands
 // OCP E4M3, block scales 2^0) in the operand layout above: each lane's 32 bytes are its
 // eight dwords, in the same K order in A and B, so the products pair up as in block_mma.
