@@ -47,6 +47,16 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base) {
 __device__ __forceinline__ v4i ld_co16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCachePolicySc1);
 }
+// Four consecutive tagged words {fp32 value, tag} from one lane (byte offset `off`, 32-byte
+// aligned), written as two 16-byte sc1 stores: each store is one request, so neither of its
+// two naturally aligned 8-byte words can tear, and a lane's four words fill one 32-byte
+// sector (an 8-byte agent-scope store costs a 32-byte memory write on its own).
+__device__ __forceinline__ void st_tagged4(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t tag, const v4f& v) {
+    const v4i lo = {(int)__float_as_uint(v[0]), (int)tag, (int)__float_as_uint(v[1]), (int)tag};
+    const v4i hi = {(int)__float_as_uint(v[2]), (int)tag, (int)__float_as_uint(v[3]), (int)tag};
+    __builtin_amdgcn_raw_buffer_store_b128(lo, r, off, 0, kCachePolicySc1);
+    __builtin_amdgcn_raw_buffer_store_b128(hi, r, off + 16u, 0, kCachePolicySc1);
+}
 
 // LDS flags shared by the wavefronts of a workgroup.  They are accessed through
 // LDS-address-space pointers with relaxed ordering: a flag update is preceded by
