@@ -38,27 +38,33 @@ def launch(plan, inp, seed):
     return d
 
 
-# (layer, T, oracle tokens, path exercised)
+# (layer, T, oracle tokens, path exercised, schedule fields (None: the default schedule))
 CASES = [
-    ("small_expert", 1, None, "one-token kernel"),
-    ("small_expert", 8, None, "general kernel, input quantised locally"),
-    ("many_tiny_expert", 4, None, "general kernel, biased routing, 256 experts"),
-    ("wide_fine", 8, [0, 7], "general kernel, input quantised once and exchanged"),
-    ("coarse", 32, [0, 31], "multi-tile kernel"),
-    ("small_expert", 64, [0, 63], "multi-tile kernel"),
-    ("many_tiny_expert", 48, [0, 47], "multi-tile kernel"),
-    ("sigmoid_h7168_tp8", 4, [0, 3], "general kernel, sigmoid routing with selection bias"),
+    ("small_expert", 1, None, "one-token kernel", None),
+    ("small_expert", 8, None, "general kernel, input quantised locally", None),
+    ("many_tiny_expert", 4, None, "general kernel, biased routing, 256 experts", None),
+    ("wide_fine", 8, [0, 7], "general kernel, input quantised once and exchanged", None),
+    ("coarse", 32, [0, 31], "multi-tile kernel", None),
+    ("small_expert", 64, [0, 63], "multi-tile kernel", None),
+    ("many_tiny_expert", 48, [0, 47], "multi-tile kernel", None),
+    ("sigmoid_h7168_tp8", 4, [0, 3], "general kernel, sigmoid routing with selection bias", None),
+    ("small_expert", 8, [0, 7], "general kernel, gate/up units dealt two at a time, down on 192 workgroups",
+     dict(up_block=2, down_grid=192)),
+    ("many_tiny_expert", 1, None, "one-token kernel, gate/up units dealt four at a time, down on 160 workgroups",
+     dict(up_block=4, down_grid=160)),
 ]
 
 
-@pytest.mark.parametrize("name,T,tokens,path", CASES)
-def test_perturbed_launches_are_bit_identical(name, T, tokens, path):
+@pytest.mark.parametrize("name,T,tokens,path,sched", CASES)
+def test_perturbed_launches_are_bit_identical(name, T, tokens, path, sched):
     inp = wl.generate(wl.config(name), T=T, seed=0, device=DEV)
     plan = mm.Plan(T, inp["H"], inp["E"], inp["I"], inp["k"], inp["renorm"], perturb=True)
     if inp["bias"] is not None:
         plan.set_router_bias(inp["bias"])
     if inp.get("policy", "softmax") == "sigmoid_bias":
         plan.set_routing(mm.ROUTING_SIGMOID_BIAS, inp["sel_bias"], inp["route_scale"])
+    if sched is not None:
+        plan.set_schedule(**sched)
     info = plan.info()
     log("case %s T=%d (%s): grid %d, multi_tile %d" % (name, T, path, info["grid"], info["multi_tile"]))
     assert bool(info["multi_tile"]) == path.startswith("multi-tile")
