@@ -140,6 +140,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
     __shared__ int f_abort, f_consumed;
     __shared__ int f_cnt[kSlotsMax];
     __shared__ int f_aq_seq[2];
+    __shared__ int f_dn_prog[kComputeWaves];   // direct down epilogues: each wave's next unfinished down unit
     __shared__ int f_rank, f_xq;                // one-token path: selections published, input quantised
 
     const int T = ONE ? 1 : p.T, E = p.E, K = p.k;   // ONE: the one-token specialisation
@@ -169,6 +170,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
         f_xq = 0;
     }
     if (tid < kSlotsMax) f_cnt[tid] = 0;
+    if (tid < kComputeWaves) f_dn_prog[tid] = tid;   // a wave's first down unit (whole units dealt round-robin)
     for (int e = tid; e < E; e += kThreads) emask[e] = 0u;
     // the flags are set before any wavefront uses them (workgroups without router rows have
     // no other barrier before their first flag accesses)
@@ -512,6 +514,27 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
         };
         bool stamped = false;
         auto handoff = [&](const v4f& acc) -> bool {   // partial sums of unit cm to the helper
+            if constexpr (NCD == 1) {
+                if (cph == 1) {
+                    // A down unit computed by this wave alone: its epilogue (routing weight,
+                    // tagged contribution) runs here instead of on the helper, and the wave's
+                    // progress (its next unit) tells the helper when an activation buffer is free.
+                    const int mu = dlo + cm, u = mu / DNE, ht = mu - u * DNE;
+                    const uint32_t tmask = act_m[u];
+                    const int c = lane & 15;
+                    MONOMOE_PERTURB(4, cm);
+                    if (c < T && ((tmask >> c) & 1u)) {
+                        const int pi = c * K + act_j[u * kTMax + c];
+                        const float w = sel_w[pi];
+                        const uint64_t th = (uint64_t)tag << 32;
+                        uint64_t* dst = p.contrib + (size_t)pi * H + ht * 16 + 4 * (lane >> 4);
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) st_co(dst + q, th | __float_as_uint(acc[q] * w));
+                    }
+                    if (lane == 0) lds_st(&f_dn_prog[wv], cm + NC);   // (after this wave's buffer reads)
+                    return true;
+                }
+            }
             const int useq = (cph == 0) ? cm : (nu + cm);
             const int slot = useq & smask;
             MONOMOE_PERTURB(1, useq);
@@ -594,7 +617,9 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
             }
             if (aborted) set_status(status, kDevTimeout);
             if (wv == 0 && lane == 0) stamp(p.stamps, wg, kStComputeDone);
+            if (NCD == 1 && wv == 0 && lane == 0) stamp(p.stamps, wg, kStDownDone);
         }
+        if (NCD == 1 && lane == 0) lds_st(&f_dn_prog[wv], 1 << 30);   // no unit left (also after an abort)
     } else if (ok) {
         // ====================== helper wavefront ======================
         bool fine = true;
@@ -736,7 +761,23 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
             lds_st(&f_aq_seq[buf], x + 1);
             return true;
         };
-        for (int j = 0; j < nd && fine; ++j) {
+        if constexpr (NCD == 1) {
+            // Down units are computed and stored by the compute wavefronts (direct epilogues):
+            // the helper only requantises each expert of the range into its buffer, once the
+            // buffer's previous expert (x - naq) has no unit left to compute.
+            for (int x = 0; x < nx && fine; ++x) {
+                if (x >= naq) {
+                    const int J = max(0, (dn_u0 + x - naq + 1) * DNE - dlo);   // first unit of expert x - naq + 1
+                    for (int w = 0; w < NC && fine; ++w)
+                        if (!wait_lds(&f_dn_prog[w], J, &f_abort, limit)) fine = false;
+                    if (!fine) break;
+                }
+                MONOMOE_PERTURB(3, x);
+                if (!prepare(x, true)) { fine = false; break; }
+                if (x == 0 && lane == 0) stamp(p.stamps, wg, kStFirstAq);
+            }
+        }
+        for (int j = 0; NCD != 1 && j < nd && fine; ++j) {
             const int m = dlo + j, u = m / DNE, ht = m - u * DNE, x = u - dn_u0;
             const int useq = nu + j, slot = useq & smask;
             while (prepared <= x) {
@@ -766,7 +807,7 @@ __global__ __launch_bounds__(kThreads) void monomoe_fused(const KParams p) {
                 for (int q = 0; q < 4; ++q) st_co(dst + q, tag_hi | __float_as_uint(y[q] * w));
             }
         }
-        if (lane == 0) stamp(p.stamps, wg, kStDownDone);
+        if (NCD != 1 && lane == 0) stamp(p.stamps, wg, kStDownDone);
         if (!fine) {
             set_status(status, kDevTimeout);
             lds_st(&f_abort, 1);

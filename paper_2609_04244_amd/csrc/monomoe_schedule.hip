@@ -46,6 +46,10 @@ enum Ev : int8_t {
     kEvPrefetch,        // helper: non-blocking preparation of expert a + 1 (two buffers)
     kEvPublishContrib,  // helper: contribution words of down unit a
     kEvWaitContrib,     // reduction of output chunk a
+    kEvDirect,          // down unit a (relative) computed by one wavefront alone: its contribution
+                        // stored by that wavefront (b: down expert, c: its slot), progress a + NC
+    kEvProgressEnd,     // compute wavefront: no down unit left (progress = infinity)
+    kEvWaitProgress,    // helper: every compute wavefront's progress >= a
     kEvEnd,
 };
 
@@ -76,6 +80,7 @@ struct Group {
     std::vector<int> barrier;     // arrivals per barrier index
     int f_rank = 0, f_xq = 0, f_consumed = 0;
     int f_aq_seq[2] = {0, 0};
+    int f_dn_prog[kComputeWaves] = {0, 1, 2, 3};   // direct down epilogues: next unfinished unit per wave
     int content[2] = {-1, -1};    // expert slot held by each activation buffer (-2: partly written)
     std::vector<int> f_cnt;       // per slot
     std::vector<int> part;        // [slot][wave]: sequence number last written (-1: none)
@@ -153,7 +158,10 @@ void build_compute(Model& M, Group& gr, int wv) {
             P.push_back({kEvWaitAq, (gr.dlo + t.m) / M.DNE - gr.dlo / M.DNE, 0, (gr.dlo + t.m) / M.DNE});
         }
     };
-    if (tasks.empty()) return;
+    if (tasks.empty()) {
+        if (M.NCD == 1) P.push_back({kEvProgressEnd, 0, 0, 0});
+        return;
+    }
     const int ring = M.ring;   // the load cursor runs this many tasks ahead of the compute cursor
     lbase(0);
     for (int s = 0; s < ring; ++s) lbase((size_t)s + 1);
@@ -166,10 +174,12 @@ void build_compute(Model& M, Group& gr, int wv) {
             const int useq = t.ph == 0 ? t.m : gr.nu + t.m;
             const int u = t.ph == 0 ? -1 : (gr.dlo + t.m) / M.DNE;
             const int x = t.ph == 0 ? -1 : u - gr.dlo / M.DNE;
-            P.push_back({kEvHandoff, useq, x, u});
+            if (t.ph == 1 && M.NCD == 1) P.push_back({kEvDirect, t.m, x, u});
+            else P.push_back({kEvHandoff, useq, x, u});
             if (i + 1 < tasks.size()) cbase(i + 1);
         }
     }
+    if (M.NCD == 1) P.push_back({kEvProgressEnd, 0, 0, 0});
 }
 
 void build_helper(Model& M, Group& gr) {
@@ -178,6 +188,16 @@ void build_helper(Model& M, Group& gr) {
         const int v = M.HP >= NC ? -1 : (j % NC);
         P.push_back({kEvConsume, j, M.NCU, v});
         P.push_back({kEvPublishAct, up_unit(gr.wg, M.G, j, M.ulb), 0, 0});
+    }
+    if (M.NCD == 1) {   // direct down epilogues: the helper only prepares each expert's buffer
+        for (int x = 0; x < gr.nx; ++x) {
+            // the buffer's previous expert (x - naq) has no unit left; the one-buffer mutation
+            // drops this wait
+            if (x >= M.naq && !(M.mutate & MONOMOE_SCHEDULE_MUTATE_PREFETCH_ONE_BUFFER))
+                P.push_back({kEvWaitProgress, std::max(0, (gr.dlo / M.DNE + x - M.naq + 1) * M.DNE - gr.dlo), 0, 0});
+            P.push_back({kEvPrepareUpTo, x, 0, 0});
+        }
+        return;
     }
     for (int j = 0; j < gr.nd; ++j) {
         const int x = (gr.dlo + j) / M.DNE - gr.dlo / M.DNE;
@@ -348,6 +368,20 @@ bool step(Model& M, Group& gr, int wv) {
         case kEvPublishContrib:
             if (M.contrib[s.a]) M.violate(kVioDuplicate);
             M.contrib[s.a] = 1;
+            break;
+        case kEvDirect:
+            if (gr.content[buf(s.b)] != s.c) M.violate(kVioBufferOverwrite);
+            if (M.contrib[gr.dlo + s.a]) M.violate(kVioDuplicate);
+            M.contrib[gr.dlo + s.a] = 1;
+            W.reading = -1;
+            gr.f_dn_prog[wv] = s.a + NC;
+            break;
+        case kEvProgressEnd:
+            gr.f_dn_prog[wv] = 1 << 30;
+            break;
+        case kEvWaitProgress:
+            for (int v = 0; v < NC; ++v)
+                if (gr.f_dn_prog[v] < s.a) return false;
             break;
         case kEvWaitContrib: {
             const int ht = s.a % (M.H / 16), c = s.a / (M.H / 16);
