@@ -28,7 +28,10 @@
 // wavefront does everything that would otherwise stall the weight stream: the gate/up
 // epilogue (SiLU(gate)*up and its store), the per-128-group requantisation of the next
 // expert's activation into LDS and the down epilogue (routing weight, contribution
-// store).
+// store).  Where a down unit is computed by one wavefront alone (I < 1024: fewer 256-deep
+// tasks per unit than wavefronts), that wavefront applies the routing weight and stores the
+// contribution itself, and publishes its progress so that the helper knows when an
+// activation buffer is free again.
 //
 // Synchronisation (Sec. 3.2, readiness-based hand-off).  Data that crosses workgroups
 // is written as 8-byte words {fp32 value, launch tag} with single-copy-atomic sc1
