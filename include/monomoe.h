@@ -321,8 +321,10 @@ int monomoe_layout(const monomoe_shape_t* shape, int topk, int kernel, int lds_t
  * issues them, with the kernel's own work-partition arithmetic: workgroup barriers, router
  * rows, the input exchange, the selection (with one token: each top-k position published as
  * it is ranked, and the compute wavefronts' quantisation counter), the partial-sum hand-off
- * slots, the requantised-activation buffers (blocking and non-blocking preparation), the
- * activation and contribution words, the output reduction.  A scheduler interleaves the
+ * slots, the requantised-activation buffers (blocking and non-blocking preparation; with
+ * single-wavefront down units, the wavefronts' own down epilogues and the progress the helper
+ * waits for before reusing a buffer), the activation and contribution words, the output
+ * reduction.  A scheduler interleaves the
  * wavefronts in a pseudo-random order drawn from `seed` (0: in index order, one event each)
  * with at most `resident` workgroups resident at once, started in index order (a new one when
  * one ends).  The result says whether every wavefront ran to its end (no deadlock) and counts
